@@ -1,0 +1,174 @@
+"""Newton-Schulz orthogonalisation, unquantised and NVFP4 (oracle; test infrastructure only).
+
+Section 2 ("Root optimizer") gives the quintic iteration
+    X_{k+1} = a X_k + b X_k (X_k^T X_k) + c X_k (X_k^T X_k)^2,
+typically five steps.  Section 3.4 gives its NVFP4 form, written with the Gram
+matrix on the left (the same polynomial, applied on the short side):
+    qX_k = Q_1x16(X_k H),           A_k = qX_k qX_k^T
+    qA_k = Q_1x16(A_k H),           qA_k^16x1 = Q_16x1(H^T A_k)
+    B_k  = b A_k + c qA_k qA_k^16x1
+    qB_k = Q_1x16(B_k H),           qX_k^16x1 = Q_16x1(H^T X_k)
+    X_{k+1} = a X_k + qB_k qX_k^16x1
+Readings taken where the paper is silent:
+* the first line's X is X_k;
+* tall matrices (rows > cols) are transposed so that the Gram matrix is the
+  short side's (m = min(rows, cols) square);
+* X_k, A_k and B_k are binary32 between products; each product is evaluated in
+  binary64 from the exact decoded operands and rounded once to binary32 (B_k
+  after its binary64 combination with b A_k);
+* A_k is exactly symmetric, so qA_k^16x1 is qA_k transposed bit for bit and
+  B_k's product is the Gram matrix of qA_k;
+* before the iteration the momentum is clipped at its p99 magnitude and
+  divided by its Frobenius norm plus eps (the Muon convention): X_0 =
+  fl32(X' * fl32(1 / (||X'||_F + eps))), the norm summed in binary64.
+"""
+from __future__ import annotations
+
+import numpy as np
+from scipy.linalg.blas import dsyrk
+
+from .quantile import clip, clip_threshold
+from .quantize import quantize
+from .rht import sylvester16, step_signs
+
+MUON_COEFFS = (3.4445, -4.7750, 2.0315)
+
+
+def gram64(d: np.ndarray) -> np.ndarray:
+    """d d^T in binary64, computed on the upper triangle and mirrored (exactly symmetric)."""
+    d = np.asarray(d, dtype=np.float64)
+    if d.shape[0] == 0:
+        return np.zeros((0, 0))
+    u = dsyrk(1.0, d, lower=0)
+    return np.triu(u) + np.triu(u, 1).T
+
+
+def f32(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float32)
+
+
+def normalise(x: np.ndarray, eps: float = 1e-7) -> np.ndarray:
+    """X_0 = fl32(X * fl32(1 / (||X||_F + eps))) with the norm summed in binary64."""
+    x = np.asarray(x, dtype=np.float32)
+    nu = np.sqrt(np.sum(np.square(x.astype(np.float64))))
+    inv = np.float32(1.0 / (nu + np.float64(np.float32(eps))))
+    return (x * inv).astype(np.float32)
+
+
+def ns_step_nvfp4(x, a, b, c, signs=None, adaptive46=True, trace=None):
+    """One NVFP4 NS step on a binary32 m x n matrix (Section 3.4 display equation)."""
+    x = np.asarray(x, dtype=np.float32)
+    a64, b64, c64 = (np.float64(np.float32(t)) for t in (a, b, c))
+    qx = quantize(x, 1, signs, adaptive46)
+    qxt = quantize(x, 0, signs, adaptive46)
+    A = f32((np.float64(qx.sg) * np.float64(qx.sg)) * gram64(qx.block_values()))
+    qa = quantize(A, 1, signs, adaptive46)
+    da = qa.block_values()
+    P = (np.float64(qa.sg) * np.float64(qa.sg)) * gram64(da)
+    B = f32(b64 * A.astype(np.float64) + c64 * P)
+    qb = quantize(B, 1, signs, adaptive46)
+    prod = qb.block_values() @ qxt.block_values().T
+    x1 = f32(a64 * x.astype(np.float64) + (np.float64(qb.sg) * np.float64(qxt.sg)) * prod)
+    if trace is not None:
+        trace.update(qx=qx, qxt=qxt, A=A, qa=qa, B=B, qb=qb)
+    return x1
+
+
+def rotate64(x: np.ndarray, signs: np.ndarray, axis: int) -> np.ndarray:
+    """Exact binary64 rotation X H (axis=1) or H^T X (axis=0) with H = diag(d) H_16 / 4."""
+    h = np.diag(signs.astype(np.float64)) @ sylvester16() / 4.0
+    x = np.asarray(x, dtype=np.float64)
+    if axis == 1:
+        r, c = x.shape
+        return (x.reshape(r, c // 16, 16) @ h).reshape(r, c)
+    r, c = x.shape
+    return np.einsum("ij,bjc->bic", h.T, x.reshape(r // 16, 16, c)).reshape(r, c)
+
+
+def ns_step_exact(x, a, b, c, signs=None):
+    """One unquantised binary64 NS step in the Section 3.4 arrangement.
+
+    With ``signs`` the rotations of Section 3.4 are applied on both sides of
+    every product (quantisation replaced by the identity); they cancel exactly
+    in exact arithmetic, which is what the placement of H must achieve.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if signs is None:
+        A = x @ x.T
+        B = b * A + c * (A @ A)
+        return a * x + B @ x
+    xh = rotate64(x, signs, 1)
+    A = xh @ xh.T
+    B = b * A + c * (rotate64(A, signs, 1) @ rotate64(A, signs, 0))
+    return a * x + rotate64(B, signs, 1) @ rotate64(x, signs, 0)
+
+
+def to_bf16(x) -> np.ndarray:
+    """Nearest bfloat16 value (8 significant bits, ties to even) of each finite input, as float64."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                      # x = m * 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0), e - 8)
+
+
+def ns_step_bf16(x, a, b, c):
+    """One step of the plain BF16 comparison path: X_k binary32 master, bf16 operands.
+
+    Xb = bf16(X_k); A = bf16(Xb Xb^T); B = bf16(b A + c A A); X_{k+1} = fl32(a X_k + B Xb),
+    each product exact in binary64 before its single rounding.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    xb = to_bf16(x)
+    A = to_bf16(gram64(xb))
+    B = to_bf16(np.float64(np.float32(b)) * A + np.float64(np.float32(c)) * gram64(A))
+    return f32(np.float64(np.float32(a)) * x.astype(np.float64) + B @ xb)
+
+
+def canonical(m: np.ndarray):
+    m = np.asarray(m, dtype=np.float32)
+    tall = m.shape[0] > m.shape[1]
+    return (np.ascontiguousarray(m.T) if tall else m), tall
+
+
+def prepare(m, clip_on=True, q=0.99, eps=1e-7):
+    """Clip (optional), orient (short side first) and normalise: returns (X_0, tall, tau)."""
+    m = np.asarray(m, dtype=np.float32)
+    tau = clip_threshold(m, q) if clip_on else np.float32(np.inf)
+    mc = clip(m, tau) if clip_on else m
+    x, tall = canonical(mc)
+    return normalise(x, eps), tall, tau
+
+
+def orthogonalize(m, coeffs, clip_on=True, q=0.99, eps=1e-7, hadamard=True,
+                  adaptive46=True, seed=0, mode="nvfp4"):
+    """Clip, normalise and run len(coeffs) NS steps; returns binary32 in the input's orientation.
+
+    mode: "nvfp4" (Section 3.4), "bf16" (plain BF16 comparison path) or "exact"
+    (binary64, no quantisation; returns float64).
+    """
+    x, tall, _ = prepare(m, clip_on, q, eps)
+    if mode == "exact":
+        x = x.astype(np.float64)
+    for k, (a, b, c) in enumerate(coeffs):
+        if mode == "nvfp4":
+            signs = step_signs(seed, k) if hadamard else None
+            x = ns_step_nvfp4(x, a, b, c, signs, adaptive46)
+        elif mode == "bf16":
+            x = ns_step_bf16(x, a, b, c)
+        elif mode == "exact":
+            x = ns_step_exact(x, a, b, c)
+        else:
+            raise ValueError(mode)
+    return np.ascontiguousarray(x.T) if tall else x
+
+
+def poly(sig, a, b, c):
+    """The scalar map one NS step applies to each singular value: a s + b s^3 + c s^5."""
+    return a * sig + b * sig ** 3 + c * sig ** 5
+
+
+def closed_form(x, coeffs):
+    """U diag(p_S(...p_1(sigma))) V^T from a binary64 SVD: what exact NS must return."""
+    u, s, vt = np.linalg.svd(np.asarray(x, dtype=np.float64), full_matrices=False)
+    for (a, b, c) in coeffs:
+        s = poly(s, a, b, c)
+    return (u * s) @ vt
