@@ -1,0 +1,195 @@
+#!/usr/bin/env python3
+"""Throughput of NVFP4 Newton-Schulz orthogonalisation on one MI355X.
+
+One "step" is one fp4root_orthogonalize call over the whole matrix set: p99
+clipping, Frobenius normalisation, five NVFP4 Newton-Schulz steps and the
+write-back, for every matrix (paper Section 3.4; Table 6 "Root" rows: isolated
+Root, five NS iterations, p99 clipping, aspect-ratio coefficients).  Inputs are
+resident in HBM before the timed region starts.
+
+Default workload: four 3B-shaped decoder blocks, 28 FP32 matrices
+(q, o 3072x3072; k, v 1024x3072; gate, up 8192x3072; down 3072x8192), seeded
+synthetic momentum (Student-t(4) entries, lognormal(0,1) row scales).
+
+Prints ONE JSON line.  Also reports, on the same line: the in-library BF16 NS
+path on the same inputs, a roofline figure for the dominant kernel measured
+with HIP events on its launch stream, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "NS-orthogonalised matrices/s + effective TFLOP/s (% MFMA peak), 3B-shaped set"
+BF16_MFMA_PEAK_TFLOPS = 2516.6
+# VALU ceiling of the exact NVFP4 product: each 16-element block product (16 MACs per
+# output) is folded into a binary64 accumulator with one conversion and one add, two
+# wave64 VALU instructions per output and block.  256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz = 39.3 T lane-ops/s -> 19.66 T output-blocks/s x 32 FLOP = 629 TFLOP/s.
+EXACT_PRODUCT_ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2.4e9 / 2 * 32 / 1e12
+
+
+def ns_flop(m: int, n: int, steps: int) -> float:
+    """Algorithmic FLOP of `steps` NS steps on an m x n matrix (m <= n), Grams exploited."""
+    return steps * (m * (m + 1) * n + m * (m + 1) * m + 2.0 * m * m * n)
+
+
+def set_flop(shapes, steps):
+    return sum(ns_flop(min(r, c), max(r, c), steps) for (r, c) in shapes)
+
+
+def time_calls(fn, warmup, iters, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(iters):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / iters
+
+
+def cpu_baseline(case, coeffs_for, steps):
+    """The oracle, as it stands, on one matrix of the workload; FLOP-scaled to the whole set."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import ns
+    from paper_2607_04422_amd import workloads
+
+    shapes = workloads.case_shapes(case)
+    # the first k projection (1024 x 3072) of the set: about 10-30 s of oracle work
+    idx = next(i for i, (_, r, c) in enumerate(shapes) if min(r, c) == 1024) if case == "block3b_x4" else 0
+    m = workloads.case_matrices(case, limit=idx + 1)[idx]
+    co = coeffs_for(m.shape[0], m.shape[1])
+    t0 = time.perf_counter()
+    ns.orthogonalize(m, co, seed=0)
+    dt = time.perf_counter() - t0
+    f_sample = ns_flop(min(m.shape), max(m.shape), steps)
+    f_set = set_flop([(r, c) for (_, r, c) in shapes], steps)
+    t_set = dt * f_set / f_sample
+    threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    return {
+        "value": len(shapes) / t_set, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
+        "sample": f"one {m.shape[0]}x{m.shape[1]} matrix of the set ({shapes[idx][0]}), clip + "
+                  f"normalise + {steps} NVFP4 NS steps in {dt:.1f} s on the host, scaled by "
+                  f"algorithmic FLOP to the {len(shapes)}-matrix set",
+        "sample_seconds": round(dt, 2),
+        "host_cpu_count": os.cpu_count(),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20, help="timed orthogonalize calls")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--case", default="block3b_x4")
+    ap.add_argument("--ns-steps", type=int, default=5)
+    ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-roofline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is a "
+                          "design note, not implemented", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_04422_amd import fp4root as F
+    from paper_2607_04422_amd import workloads
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    F.load()
+    dev = torch.device("cuda:0")
+    shapes = workloads.case_shapes(args.case)
+    mats = workloads.case_matrices(args.case)
+    inputs = [torch.from_numpy(m).to(dev) for m in mats]
+    del mats
+    S = args.ns_steps
+    flop = set_flop([(r, c) for (_, r, c) in shapes], S)
+
+    orth = F.Orthogonalizer(inputs, steps=S, flags=F.F_DEFAULT, clip_quantile=0.99, eps=1e-7, seed=0)
+    orth()
+    torch.cuda.synchronize()
+    if orth.status() != 0:
+        print(json.dumps({"error": f"device status {orth.status()}"}))
+        sys.exit(1)
+    t_step = time_calls(orth, args.warmup, args.steps, torch)
+    value = len(shapes) / t_step
+    tflops = flop / t_step / 1e12
+
+    roofline = None
+    if not args.no_roofline:
+        F.fp4root_timer_reset()
+        F.fp4root_timer_enable(True)
+        for _ in range(args.steps):
+            orth()
+        torch.cuda.synchronize()
+        F.fp4root_timer_enable(False)
+        per_kernel = {k: F.fp4root_timer_read(k) for k in (0, 1, 2)}
+        F.fp4root_timer_reset()
+        ms2, n2, fl2 = per_kernel[2]            # the update product X <- a X + qB qXt^T
+        achieved = fl2 / (ms2 / 1e3) / 1e12 if ms2 > 0 else 0.0
+        peak = EXACT_PRODUCT_ALU_PEAK_TFLOPS
+        roofline = {
+            "kernel": "k_gemm_fp4<update X> (exact NVFP4 product, f16 MFMA per block, f64 accumulation)",
+            "bound": "alu", "achieved": round(achieved, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "avg_launch_ms": round(ms2 / max(n2, 1), 4), "launches": n2,
+            "all_products_tflops": round(sum(v[2] for v in per_kernel.values()) /
+                                         (sum(v[0] for v in per_kernel.values()) / 1e3) / 1e12, 2),
+            "products_share_of_step": round(sum(v[0] for v in per_kernel.values()) / args.steps /
+                                            (t_step * 1e3), 4),
+            "per_kernel_tflops": {str(k): round(v[2] / (v[0] / 1e3) / 1e12, 2) if v[0] else 0.0
+                                  for k, v in per_kernel.items()},
+        }
+
+    bf16 = None
+    if not args.no_bf16:
+        orth16 = F.Orthogonalizer(inputs, steps=S, flags=F.F_CLIP | F.F_BF16_PATH, clip_quantile=0.99,
+                                  eps=1e-7, seed=0)
+        t16 = time_calls(orth16, args.warmup, args.steps, torch)
+        bf16 = {"ms_per_step": round(t16 * 1e3, 3), "matrices_per_s": round(len(shapes) / t16, 2),
+                "tflops_effective": round(flop / t16 / 1e12, 2),
+                "pct_bf16_peak": round(100 * flop / t16 / 1e12 / BF16_MFMA_PEAK_TFLOPS, 2),
+                "nvfp4_speedup_vs_bf16": round(t16 / t_step, 3)}
+        del orth16
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(args.case, lambda r, c: F.fp4root_default_coeffs(r, c, S), S)
+
+    line = {
+        "metric": METRIC, "value": round(value, 3), "unit": "matrices/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_step * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "nvfp4 operands; f16 MFMA exact block products; f64 accumulation",
+        "data": "synthetic",
+        "config": {"workload": f"{args.case}: {workloads.CASES[args.case]}", "matrices": len(shapes),
+                   "ns_steps": S, "clip_quantile": 0.99, "flags": "clip+hadamard+adaptive46",
+                   "algorithmic_tflop_per_step": round(flop / 1e12, 3), "parallelism": "single GPU"},
+        "tflops_effective": round(tflops, 2),
+        "pct_bf16_mfma_peak": round(100 * tflops / BF16_MFMA_PEAK_TFLOPS, 2),
+        "roofline": roofline,
+        "bf16_path": bf16,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,199 @@
+/*
+ * fp4root -- NVFP4 Newton-Schulz orthogonalisation ("Q-Root") on AMD gfx950.
+ *
+ * C ABI of libfp4root.so.  Every entry point takes plain pointers and sizes;
+ * device pointers are HIP device memory, host pointers are ordinary memory.
+ * `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *
+ * The method (paper: "Full-Stack FP4", Section 3.4 and its display equation;
+ * Section 2 "NVFP4 format" and "Root optimizer"):
+ *   - momentum M (rows x cols, FP32) is clipped at its 0.99 quantile of |M|
+ *     (Section 3.4 "p99 outlier clipping"; Table 8 "Root quantile ratio 0.99"),
+ *     oriented so the short side comes first (X = M^T when rows > cols) and
+ *     divided by its Frobenius norm plus eps;
+ *   - S Newton-Schulz steps X <- a X + b (X X^T) X + c (X X^T)^2 X run with every
+ *     matrix product on NVFP4 operands:
+ *         qX = Q1x16(X H), A = qX qX^T, qA = Q1x16(A H),
+ *         B = b A + c qA qA^T, qB = Q1x16(B H), qXt = Q16x1(H^T X),
+ *         X <- a X + qB qXt
+ *     with H a fresh random 16x16 Hadamard transform per step, RTN rounding
+ *     and adaptive 4/6 block scaling;
+ *   - the result is returned in the input's orientation.
+ *
+ * NVFP4 tensor layout produced by fp4root_quantize (Section 2 "NVFP4 format"):
+ *   codes:  one 4-bit code per element, bit 3 = sign, bits 0-2 = E2M1 magnitude
+ *           index into {0, 0.5, 1, 1.5, 2, 3, 4, 6}; two codes per byte, element
+ *           2j in the low nibble;
+ *   scales: one E4M3FN byte (OCP FP8, bias 7, max 448) per 16-element block;
+ *   tensor_scale: one FP32 s_g per matrix; decode x = code * scale * s_g.
+ *   The quantiser's readings where the paper is silent: s_g = amax/2688 over the
+ *   rotated matrix; block scale E4M3_RNE(min(bmax / (M s_g), 448)) for M = 6, and
+ *   also M = 4 with adaptive 4/6 (kept iff its float64 squared error over the
+ *   block is strictly smaller); element code E2M1_RNE(min(|u| / (s s_g), 6)).
+ *
+ * Products are evaluated exactly: each 16-element block product is exact in
+ * FP32 and blocks are accumulated in FP64, so each product is the binary32
+ * rounding of its (binary64) exact value.
+ *
+ * Errors: argument, shape and workspace errors are returned synchronously and
+ * nothing is launched.  Non-finite input values are detected on the device and
+ * recorded in a status word inside the workspace; read it with
+ * fp4root_device_status().  The library allocates no device memory: every
+ * buffer is the caller's, the workspace included.  Calls are asynchronous with
+ * respect to the host; concurrent calls must use distinct workspaces.
+ */
+#ifndef FP4ROOT_H
+#define FP4ROOT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+enum {
+  FP4ROOT_OK = 0,
+  FP4ROOT_ERR_INVALID_ARG = -1, /* null pointer, bad count, bad flag or parameter */
+  FP4ROOT_ERR_SHAPE = -2,       /* a dimension is not a positive multiple of 16, or strides too small */
+  FP4ROOT_ERR_WORKSPACE = -3,   /* workspace null or smaller than the size query returned */
+  FP4ROOT_ERR_NONFINITE = -4,   /* (device status) a NaN or Inf was met in an input */
+  FP4ROOT_ERR_HIP = -5,         /* a HIP runtime call failed */
+  FP4ROOT_ERR_UNSUPPORTED = -6  /* a combination this build does not implement */
+};
+
+/* Flags. */
+enum {
+  FP4ROOT_F_CLIP = 1u,        /* clip at the clip_quantile of |M| before anything else        */
+  FP4ROOT_F_HADAMARD = 2u,    /* apply the random 16x16 Hadamard rotation (Section 3.4)      */
+  FP4ROOT_F_ADAPTIVE46 = 4u,  /* adaptive 4/6 block scaling (Section 3.4)                    */
+  FP4ROOT_F_BF16_PATH = 8u,   /* plain BF16 Newton-Schulz instead of NVFP4 (comparison path) */
+  FP4ROOT_F_DEFAULT = 7u      /* CLIP | HADAMARD | ADAPTIVE46: the paper's route             */
+};
+
+/* One matrix of a batched orthogonalisation.  in/out are device pointers to
+ * row-major FP32 matrices of rows x cols with leading dimensions ld_in/ld_out
+ * (in elements, >= cols).  in and out may be the same buffer with the same ld. */
+typedef struct {
+  const float* in;
+  float* out;
+  int64_t rows, cols, ld_in, ld_out;
+} fp4root_matrix;
+
+/* Newton-Schulz configuration (host memory). */
+typedef struct {
+  int32_t steps;        /* number of NS steps S (>= 0); the paper uses 5 (Section 2)       */
+  const float* coeffs;  /* host array of steps*3 floats (a_k, b_k, c_k), or NULL for the
+                           library's default table, chosen per matrix by aspect ratio     */
+  uint32_t flags;       /* FP4ROOT_F_*                                                     */
+  float clip_quantile;  /* quantile ratio q in [0, 1]; the paper's value is 0.99          */
+  float eps;            /* Frobenius normalisation guard; 1e-7                             */
+  uint64_t seed;        /* seed of the per-step Hadamard signs (SplitMix64 output k+1)     */
+} fp4root_ns_config;
+
+/* Optional per-step export of intermediates (device pointers, caller-owned; any
+ * member may be NULL to skip it).  Layouts as for fp4root_quantize; A and B are
+ * FP32 m x m row-major per matrix, batch stride m*m. */
+typedef struct {
+  uint8_t *qx_codes, *qx_scales;    float* qx_sg;    /* Q1x16(X H):   m x n/2, m x n/16 */
+  uint8_t *qxt_codes, *qxt_scales;  float* qxt_sg;   /* Q16x1(H^T X): n x m/2, n x m/16 */
+  float* A;                                          /* qX qX^T                         */
+  uint8_t *qa_codes, *qa_scales;    float* qa_sg;    /* Q1x16(A H):   m x m/2, m x m/16 */
+  float* B;                                          /* b A + c qA qA^T                 */
+  uint8_t *qb_codes, *qb_scales;    float* qb_sg;    /* Q1x16(B H)                      */
+} fp4root_ns_trace;
+
+/* ---- size queries (host only, no GPU work) -------------------------------- */
+
+/* Workspace bytes fp4root_quantize needs for this batch (at least 256). */
+size_t fp4root_quantize_workspace(int64_t batch, int64_t rows, int64_t cols, uint32_t flags);
+
+/* Workspace bytes fp4root_ns_step needs for a batch of m x n matrices. */
+size_t fp4root_ns_step_workspace(int64_t batch, int64_t m, int64_t n, uint32_t flags);
+
+/* Workspace bytes fp4root_orthogonalize needs for this matrix list and config.
+ * Returns 0 when the arguments are invalid (the call would fail with an error). */
+size_t fp4root_orthogonalize_workspace(const fp4root_matrix* mats, int64_t count,
+                                       const fp4root_ns_config* cfg);
+
+/* ---- the three operations ------------------------------------------------- */
+
+/* NVFP4 quantiser (Section 2 "NVFP4 format"; Section 3.4, all quantisations RTN
+ * with adaptive 4/6; clipping of Section 3.4 when FP4ROOT_F_CLIP is set).
+ *   x:     device, batch matrices of rows x cols FP32, row stride ld, matrix
+ *          stride batch_stride (elements);
+ *   axis:  1 = blocks of 16 along a row (Q1x16); codes are batch x rows x cols/2
+ *          bytes, scales batch x rows x cols/16;
+ *          0 = blocks of 16 down a column (Q16x1), stored transposed: codes
+ *          batch x cols x rows/2, scales batch x cols x rows/16;
+ *   flags: FP4ROOT_F_CLIP | FP4ROOT_F_HADAMARD | FP4ROOT_F_ADAPTIVE46;
+ *   clip_quantile: used with FP4ROOT_F_CLIP (threshold per matrix);
+ *   seed, step: the Hadamard signs are those of NS step `step` under `seed`;
+ *   codes, scales, tensor_scale (batch floats): device outputs;
+ *   clip_threshold: optional device output (batch floats) of the thresholds, or NULL.
+ * rows and cols must be multiples of 16. */
+int fp4root_quantize(const float* x, int64_t batch, int64_t rows, int64_t cols, int64_t ld,
+                     int64_t batch_stride, int axis, uint32_t flags, float clip_quantile,
+                     uint64_t seed, int32_t step, uint8_t* codes, uint8_t* scales,
+                     float* tensor_scale, float* clip_threshold, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* One NVFP4 Newton-Schulz step (Section 3.4 display equation), in place.
+ *   x: device, batch matrices m x n FP32, rows contiguous (row stride n), matrix
+ *      stride batch_stride >= m*n; any m, n that are multiples of 16 (m <= n is
+ *      the efficient orientation: the Gram matrix is m x m);
+ *   a, b, c: this step's coefficients; flags: HADAMARD | ADAPTIVE46 | BF16_PATH;
+ *   seed, step: select the Hadamard signs; trace: optional export, or NULL. */
+int fp4root_ns_step(float* x, int64_t batch, int64_t m, int64_t n, int64_t batch_stride,
+                    float a, float b, float c, uint32_t flags, uint64_t seed, int32_t step,
+                    const fp4root_ns_trace* trace, void* ws, size_t ws_bytes, void* stream);
+
+/* Batched NVFP4 Root orthogonalisation of `count` matrices (Section 3.4):
+ * clip, orient short side first, normalise, cfg->steps NS steps, write back in
+ * the input orientation.  Matrices of equal (short, long) shape are batched
+ * into the same kernel launches. */
+int fp4root_orthogonalize(const fp4root_matrix* mats, int64_t count,
+                          const fp4root_ns_config* cfg, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* ---- helpers --------------------------------------------------------------- */
+
+/* The library's default per-step coefficients for a rows x cols matrix:
+ * writes steps*3 floats to out3 (host).  The paper uses Root's shape-dependent
+ * coefficients without printing them; this table is this library's own fit,
+ * keyed by the aspect ratio round(long/short) clamped to [1, 4]. */
+int fp4root_default_coeffs(int64_t rows, int64_t cols, int32_t steps, float* out3);
+
+/* Waits for `stream`, then returns FP4ROOT_OK or the first device-detected error
+ * recorded in the workspace `ws` by the last call that used it. */
+int fp4root_device_status(const void* ws, void* stream);
+
+/* Static description of a return code. */
+const char* fp4root_status_string(int status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int fp4root_version(void);
+
+/* ---- kernel timing for measurement harnesses -------------------------------
+ * While enabled, each matrix-product kernel the library launches is bracketed
+ * by two HIP events recorded on the stream it is launched on.  Kernel ids:
+ * 0 = Gram product A = qX qX^T, 1 = Gram product with the B epilogue,
+ * 2 = update product X <- a X + qB qXt^T (for the BF16 path: the same three
+ * products on bf16 operands).  Not for production use: recording costs a few
+ * microseconds per launch. */
+int fp4root_timer_enable(int on);
+
+/* Waits for the recorded launches of `kernel` (-1 = all) and returns their
+ * summed kernel time in milliseconds, their number and their algorithmic FLOP
+ * (symmetric products: m(m+1)k; others: 2mnk; per matrix). */
+int fp4root_timer_read(int kernel, double* ms, int64_t* launches, double* flop);
+
+/* Drops every record (keeps the events for reuse). */
+int fp4root_timer_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP4ROOT_H */

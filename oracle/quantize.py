@@ -60,8 +60,13 @@ class NVFP4:
 
 
 def quantize(x: np.ndarray, axis: int = 1, signs: np.ndarray | None = None,
-             adaptive46: bool = True) -> NVFP4:
-    """Quantise a float32 matrix to NVFP4 along ``axis`` (see module docstring)."""
+             adaptive46: bool = True, rows: np.ndarray | None = None) -> NVFP4:
+    """Quantise a float32 matrix to NVFP4 along ``axis`` (see module docstring).
+
+    ``rows`` (optional) selects rows of the blocked layout (rows of x for axis 1,
+    columns of x for axis 0) to encode; the tensor scale still comes from the
+    whole matrix, so each selected row equals the same row of the full result.
+    """
     x = np.asarray(x, dtype=np.float32)
     if x.ndim != 2:
         raise ValueError("quantize expects a matrix")
@@ -71,15 +76,21 @@ def quantize(x: np.ndarray, axis: int = 1, signs: np.ndarray | None = None,
         x = x.T
     elif axis != 1:
         raise ValueError("axis must be 0 or 1")
-    rows, cols = x.shape
+    nrows, cols = x.shape
     if cols % 16:
         raise ValueError("blocked axis must be a multiple of 16")
-    blocks = np.ascontiguousarray(x).reshape(rows, cols // 16, 16)
+    blocks = np.ascontiguousarray(x).reshape(nrows, cols // 16, 16)
     u = rotate_blocks_f32(blocks, signs) if signs is not None else blocks.astype(np.float32)
     neg = np.signbit(u)
     mag = np.abs(u)
     amax = np.float32(mag.max()) if mag.size else np.float32(0.0)
     sg = np.float32(amax / SG_DIVISOR)
+    if rows is not None:
+        rows_idx = np.asarray(rows, dtype=np.int64)
+        u, neg, mag = u[rows_idx], neg[rows_idx], mag[rows_idx]
+        rows = len(rows_idx)
+    else:
+        rows = u.shape[0]
     nblk = rows * (cols // 16)
     if sg == 0:
         codes = (neg.astype(np.uint8) << 3).reshape(rows, cols)

@@ -1,0 +1,369 @@
+// Matrix products of the Newton-Schulz step on gfx950 MFMA.
+//
+// All three products of a step (Section 3.4 display equation) have both
+// operands contiguous along the contraction index:
+//   A = qX qX^T        (K = n, symmetric: upper tiles only, mirrored)
+//   B = b A + c qA qA^T (K = m, symmetric; epilogue reads A, may overwrite it)
+//   X <- a X + qB qXt^T (K = m; epilogue reads X_k and writes X_{k+1} in place)
+//
+// NVFP4 operands (exact bridge): codes and E4M3 scales are decoded to f16
+// while staging into LDS (q * s needs at most 6 significant bits and lies in
+// [2^-10, 2688], so it is exact in f16).  One MFMA 32x32x16 covers exactly one
+// 16-element block: all its products are integer multiples of s_a s_b / 4 with
+// |sum| < 2^19 of those units, so the MFMA result (accumulator input 0) is the
+// exact block sum.  Block sums are accumulated in binary64 and the epilogue
+// forms the output in binary64 and rounds once to binary32, so every product
+// equals the binary32 rounding of its exact value.
+//
+// BF16 operands (comparison path): standard MFMA 32x32x16 bf16 with binary32
+// accumulation across the whole K loop.
+#include "device.h"
+#include "internal.h"
+
+namespace fp4r {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128;        // output tile rows
+constexpr int BN = 128;        // output tile cols
+constexpr int KS = 64;         // K per LDS stage (4 NVFP4 blocks)
+constexpr int kThreads = 256;  // 4 waves in a 2 x 2 grid, 64 x 64 outputs each
+
+// LDS element (row, k) of a 128 x 64 16-bit tile: 16-byte chunks XOR-swizzled by row.
+FP4R_DEV int lds_idx(int row, int chunk) { return row * KS + ((chunk ^ (row & 7)) << 3); }
+
+// Output tile coordinates.  Symmetric products enumerate the upper triangle
+// row by row; others are row-major over (tiles_m x tiles_n).
+FP4R_DEV void tile_coords(int64_t t, int tiles_m, int tiles_n, bool sym, int& tm, int& tn) {
+  if (!sym) {
+    tm = (int)(t / tiles_n);
+    tn = (int)(t % tiles_n);
+    return;
+  }
+  int r = 0;
+  int64_t left = t;
+  while (left >= tiles_n - r) {
+    left -= tiles_n - r;
+    ++r;
+  }
+  tm = r;
+  tn = r + (int)left;
+}
+
+// ---------------------------------------------------------------------------
+// NVFP4 operand staging.
+
+struct Fp4Stage {
+  uint2 codes[2];
+  uint32_t scales[2];
+};
+
+FP4R_DEV void fp4_load(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t K, int64_t row0,
+                       int stage, Fp4Stage& s) {
+  const int r = threadIdx.x >> 1, h = threadIdx.x & 1;
+  const int64_t grow = row0 + r;
+  const int64_t nkb = K / 16;
+  const uint8_t* codes = op.codes + mat * op.codes_bstride + grow * (K / 2);
+  const uint8_t* scales = op.scales + mat * op.scales_bstride + grow * nkb;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int64_t kb = (int64_t)stage * 4 + 2 * h + j;
+    if (grow < rows && kb < nkb) {
+      s.codes[j] = *reinterpret_cast<const uint2*>(codes + kb * 8);
+      s.scales[j] = scales[kb];
+    } else {
+      s.codes[j] = make_uint2(0u, 0u);
+      s.scales[j] = 0u;
+    }
+  }
+}
+
+template <int SEL>
+FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
+  // two E2M1 codes (low nibble first) -> two f16, then the exact product with the block scale
+  const f16x2 q = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, SEL);
+  return q * s2;
+}
+
+FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage& s) {
+  const int r = threadIdx.x >> 1, h = threadIdx.x & 1;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const _Float16 sv = (_Float16)e4m3_value(s.scales[j]);
+    const f16x2 s2 = {sv, sv};
+    const uint32_t w[2] = {s.codes[j].x, s.codes[j].y};
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      f16x8 v;
+      const f16x2 p0 = fp4_pair<0>(w[half], s2), p1 = fp4_pair<1>(w[half], s2);
+      const f16x2 p2 = fp4_pair<2>(w[half], s2), p3 = fp4_pair<3>(w[half], s2);
+      v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
+      v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
+      const int chunk = (2 * h + j) * 2 + half;
+      *reinterpret_cast<f16x8*>(lds + lds_idx(r, chunk)) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact NVFP4 product.
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n,
+                                                       int64_t tiles_per_mat) {
+  __shared__ _Float16 lds[2][2][BM * KS];
+  constexpr bool kSym = MODE != kModeUpdateX;
+  const int64_t mat = blockIdx.x / tiles_per_mat;
+  int tm, tn;
+  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
+  const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int64_t nkb = g.K / 16;
+  const int nstages = (int)((nkb + 3) / 4);
+
+  double acc[2][2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0;
+
+  Fp4Stage sa, sb;
+  fp4_load(g.a, mat, g.M, g.K, row0, 0, sa);
+  fp4_load(g.b, mat, g.N, g.K, col0, 0, sb);
+  fp4_store(lds[0][0], sa);
+  fp4_store(lds[0][1], sb);
+  __syncthreads();
+
+  const f32x16 zero = {};
+  for (int s = 0; s < nstages; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nstages) {
+      fp4_load(g.a, mat, g.M, g.K, row0, s + 1, sa);
+      fp4_load(g.b, mat, g.N, g.K, col0, s + 1, sb);
+    }
+    const _Float16* la = lds[buf][0];
+    const _Float16* lb = lds[buf][1];
+    const int kbs = (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4);
+    for (int kb = 0; kb < kbs; ++kb) {
+      const int chunk = kb * 2 + (lane >> 5);
+      f16x8 af[2], bfr[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx(wm * 64 + i * 32 + (lane & 31), chunk));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx(wn * 64 + j * 32 + (lane & 31), chunk));
+      f32x16 p[2][2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
+    }
+    if (s + 1 < nstages) {
+      fp4_store(lds[buf ^ 1][0], sa);
+      fp4_store(lds[buf ^ 1][1], sb);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: binary64 formula, one rounding to binary32
+  const double sga = (double)g.sc[mat].sg[g.slot_a], sgb = (double)g.sc[mat].sg[g.slot_b];
+  const double alpha = sga * sgb;   // exact: product of two binary32 values
+  const double ca = (double)g.ca, cb = (double)g.cb, cc = (double)g.cc;
+  float* out = g.out + mat * g.out_bstride;
+  const float* aux = g.aux ? g.aux + mat * g.out_bstride : nullptr;
+  const bool mirror = kSym && tm != tn;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t r = row0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int64_t c = col0 + wn * 64 + j * 32 + (lane & 31);
+        if (r < g.M && c < g.N) {
+          double v = alpha * acc[i][j][e];
+          if (MODE == kModeGramB) v = cb * (double)aux[r * g.N + c] + cc * v;
+          if (MODE == kModeUpdateX) v = ca * (double)aux[r * g.N + c] + v;
+          const float f = (float)v;
+          out[r * g.N + c] = f;
+          if (mirror) out[c * g.N + r] = f;
+        }
+      }
+}
+
+hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st) {
+  const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
+  const bool sym = mode != kModeUpdateX;
+  const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
+  const dim3 grid((uint32_t)(per * g.batch));
+  switch (mode) {
+    case kModeGramA:
+      hipLaunchKernelGGL(k_gemm_fp4<kModeGramA>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      break;
+    case kModeGramB:
+      hipLaunchKernelGGL(k_gemm_fp4<kModeGramB>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      break;
+    default:
+      hipLaunchKernelGGL(k_gemm_fp4<kModeUpdateX>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// BF16 comparison product.
+
+struct Bf16Stage {
+  uint4 v[4];
+};
+
+FP4R_DEV void bf16_load(const uint16_t* base, int64_t rows, int64_t K, int64_t row0, int stage,
+                        Bf16Stage& s) {
+  const int chunk = threadIdx.x & 7;
+  const int64_t k = (int64_t)stage * KS + chunk * 8;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t grow = row0 + (threadIdx.x >> 3) + 32 * q;
+    if (grow < rows && k < K)
+      s.v[q] = *reinterpret_cast<const uint4*>(base + grow * K + k);
+    else
+      s.v[q] = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+FP4R_DEV void bf16_store(uint16_t* lds, const Bf16Stage& s) {
+  const int chunk = threadIdx.x & 7;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = (threadIdx.x >> 3) + 32 * q;
+    *reinterpret_cast<uint4*>(lds + lds_idx(r, chunk)) = s.v[q];
+  }
+}
+
+FP4R_DEV uint16_t to_bf16(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+FP4R_DEV float from_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void k_gemm_bf16(GemmBf16Args g, int tiles_m, int tiles_n,
+                                                        int64_t tiles_per_mat) {
+  __shared__ uint16_t lds[2][2][BM * KS];
+  constexpr bool kSym = MODE != kModeUpdateX;
+  const int64_t mat = blockIdx.x / tiles_per_mat;
+  int tm, tn;
+  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
+  const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int nstages = (int)((g.K + KS - 1) / KS);
+  const uint16_t* A = g.a + mat * g.a_bstride;
+  const uint16_t* B = g.b + mat * g.b_bstride;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  Bf16Stage sa, sb;
+  bf16_load(A, g.M, g.K, row0, 0, sa);
+  bf16_load(B, g.N, g.K, col0, 0, sb);
+  bf16_store(lds[0][0], sa);
+  bf16_store(lds[0][1], sb);
+  __syncthreads();
+  for (int s = 0; s < nstages; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nstages) {
+      bf16_load(A, g.M, g.K, row0, s + 1, sa);
+      bf16_load(B, g.N, g.K, col0, s + 1, sb);
+    }
+    const uint16_t* la = lds[buf][0];
+    const uint16_t* lb = lds[buf][1];
+    const int64_t krem = g.K - (int64_t)s * KS;
+    const int kbs = (int)(krem < KS ? krem / 16 : 4);
+    for (int kb = 0; kb < kbs; ++kb) {
+      const int chunk = kb * 2 + (lane >> 5);
+      bf16x8 af[2], bfr[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(la + lds_idx(wm * 64 + i * 32 + (lane & 31), chunk));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8*>(lb + lds_idx(wn * 64 + j * 32 + (lane & 31), chunk));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (s + 1 < nstages) {
+      bf16_store(lds[buf ^ 1][0], sa);
+      bf16_store(lds[buf ^ 1][1], sb);
+    }
+    __syncthreads();
+  }
+
+  const bool mirror = kSym && tm != tn;
+  uint16_t* o16 = g.out16 + mat * g.out16_bstride;
+  const uint16_t* aux16 = g.aux16 ? g.aux16 + mat * g.out16_bstride : nullptr;
+  float* X = g.x ? g.x + mat * g.x_bstride : nullptr;
+  uint16_t* o16t = g.out16t ? g.out16t + mat * g.out16t_bstride : nullptr;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t r = row0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int64_t c = col0 + wn * 64 + j * 32 + (lane & 31);
+        if (r < g.M && c < g.N) {
+          float v = acc[i][j][e];
+          if (MODE == kModeGramB) v = g.cb * from_bf16(aux16[r * g.N + c]) + g.cc * v;
+          if (MODE == kModeUpdateX) {
+            v = g.ca * X[r * g.N + c] + v;
+            X[r * g.N + c] = v;
+            const uint16_t h = to_bf16(v);
+            o16[r * g.N + c] = h;
+            o16t[c * g.M + r] = h;
+          } else {
+            const uint16_t h = to_bf16(v);
+            o16[r * g.N + c] = h;
+            if (mirror) o16[c * g.N + r] = h;
+          }
+        }
+      }
+}
+
+hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st) {
+  const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
+  const bool sym = mode != kModeUpdateX;
+  const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
+  const dim3 grid((uint32_t)(per * g.batch));
+  switch (mode) {
+    case kModeGramA:
+      hipLaunchKernelGGL(k_gemm_bf16<kModeGramA>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      break;
+    case kModeGramB:
+      hipLaunchKernelGGL(k_gemm_bf16<kModeGramB>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      break;
+    default:
+      hipLaunchKernelGGL(k_gemm_bf16<kModeUpdateX>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fp4r

@@ -1,0 +1,154 @@
+// Internal launcher interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fp4r {
+
+// Device status bits (kept in the first word of every workspace).
+constexpr uint32_t kStatusNonFinite = 1u;
+
+// ---------------------------------------------------------------------------
+// Matrix lists for the stages that read caller matrices (clipping, copies).
+constexpr int kMaxChunk = 32;
+
+struct MatDesc {
+  const float* in;     // caller matrix, row-major
+  float* out;          // caller output (copy-out stage) or nullptr
+  int64_t rows, cols, ld_in, ld_out;
+  int64_t lo;          // quantile order statistic index floor(q (N - 1))
+  double frac;         // q (N - 1) - lo
+  int64_t tile_begin;  // first flat block index of this matrix in a launch
+};
+
+struct MatChunk {
+  MatDesc m[kMaxChunk];
+  int count;
+  int64_t total_tiles;
+};
+
+// Per-matrix scalars kept in the workspace (one struct per matrix).
+struct MatScalars {
+  uint32_t amax[4];      // bit patterns: X along n, X along m, A, B
+  float sg[4];           // tensor scales derived from amax
+  float tau;             // clip threshold (+inf without clipping)
+  float inv_norm;        // 1 / (||X'||_F + eps)
+  uint32_t sel_prefix[2];  // radix select state for ranks lo and lo + 1
+  uint32_t sel_rank[2];
+  uint32_t pad[2];
+};
+
+constexpr int kSlotXn = 0, kSlotXm = 1, kSlotA = 2, kSlotB = 3;
+
+// Radix select histogram: [2 ranks][2048 bins] per matrix.
+constexpr int kHistBins = 2048;
+constexpr int kPrepRowsPerBlock = 8;
+
+// ---------------------------------------------------------------------------
+// Launchers (all asynchronous on `st`; return hipSuccess or the launch error).
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t n, hipStream_t st);
+
+// Quantile of |x| per matrix in the chunk; writes sc[i].tau (ranks lo, lo+1).
+// hist: chunk.count * 2 * kHistBins words of scratch.  status: device word.
+hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* hist,
+                                 uint32_t* status, hipStream_t st);
+
+// Frobenius norm of the clipped matrices: sc[i].inv_norm = fl32(1/(||.|| + eps)).
+// partial: chunk.total_tiles doubles of scratch.
+hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, float eps,
+                           hipStream_t st);
+
+// Canonical copy: X_b (m x n, m = min(rows, cols)) = fl32(clamp(M, tau) * inv_norm),
+// transposed when rows > cols.  x: base of the group's canonical buffer, matrix b
+// of the chunk at x + (first + b) * x_bstride.
+hipError_t launch_prep_copy(const MatChunk& ch, const MatScalars* sc, float* x,
+                            int64_t x_bstride, hipStream_t st);
+
+// Copy-out: caller out (rows x cols) from canonical X (transposed when rows > cols).
+hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride,
+                           hipStream_t st);
+
+// Uniform batch view of FP32 matrices.
+struct Batch {
+  const float* x;
+  int64_t batch, rows, cols, ld, bstride;
+};
+
+// NVFP4 output view (axis 1: rows x cols/2 codes; axis 0: cols x rows/2 codes).
+struct QOut {
+  uint8_t* codes;
+  uint8_t* scales;
+  int64_t codes_bstride, scales_bstride;
+};
+
+// amax over rotated 16-blocks along `axis`; atomically maxes into
+// sc[b].amax[slot].  tau: clamp each element to +-sc[b].tau first when clip != 0.
+hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
+                       MatScalars* sc, int slot, uint32_t* status, hipStream_t st);
+
+// Encode with the tensor scale derived from sc[b].amax[slot]; writes sc[b].sg[slot]
+// and, when tensor_scale != nullptr, tensor_scale[b].
+hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
+                         bool adaptive46, MatScalars* sc, int slot, const QOut& out,
+                         float* tensor_scale, hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// GEMMs (all operands K-contiguous: C[i][j] = sum_k A[i][k] B[j][k]).
+
+enum GemmMode { kModeGramA = 0, kModeGramB = 1, kModeUpdateX = 2 };
+
+struct Fp4Operand {
+  const uint8_t* codes;   // [rows][K/2]
+  const uint8_t* scales;  // [rows][K/16]
+  int64_t codes_bstride, scales_bstride;
+};
+
+struct GemmFp4Args {
+  Fp4Operand a, b;
+  int64_t M, N, K, batch;
+  const MatScalars* sc;   // tensor scales per matrix
+  int slot_a, slot_b;
+  float* out;             // FP32 [M][N] per matrix (ld = N)
+  int64_t out_bstride;
+  const float* aux;       // kModeGramB: A (may equal out); kModeUpdateX: X_k (may equal out)
+  float ca, cb, cc;
+};
+
+// NVFP4 product with exact block sums accumulated in binary64.
+// kModeGramA / kModeGramB compute upper-triangle tiles only and mirror them.
+hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st);
+
+struct GemmBf16Args {
+  const uint16_t* a;      // bf16 [M][K] per matrix
+  const uint16_t* b;      // bf16 [N][K] per matrix
+  int64_t a_bstride, b_bstride;
+  int64_t M, N, K, batch;
+  uint16_t* out16;        // kModeGramA/B: bf16 [M][N] (ld = N); kModeUpdateX: Xb [M][N]
+  int64_t out16_bstride;
+  uint16_t* out16t;       // kModeUpdateX: Xbt [N][M]
+  int64_t out16t_bstride;
+  float* x;               // kModeUpdateX: FP32 X in place [M][N]
+  int64_t x_bstride;
+  const uint16_t* aux16;  // kModeGramB: bf16 A (may equal out16)
+  float ca, cb, cc;
+};
+
+// Plain BF16 product with FP32 accumulation (the comparison path).
+hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st);
+
+// Xb = bf16(X), Xbt = bf16(X)^T for a batch of m x n FP32 matrices.
+hipError_t launch_cast_bf16(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
+                            uint16_t* xb, uint16_t* xbt, int64_t b_bstride, hipStream_t st);
+
+// Zero the amax slots of n scalar records; `full` also resets tensor scales,
+// tau (+inf) and inv_norm (1).
+hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, bool full, hipStream_t st);
+
+// out[i] = sc[i].tau (which = 0) or sc[i].sg[slot] (which = 1).
+hipError_t launch_export_scalar(const MatScalars* sc, int64_t n, int which, int slot, float* out,
+                                hipStream_t st);
+
+}  // namespace fp4r

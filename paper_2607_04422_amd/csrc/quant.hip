@@ -1,0 +1,504 @@
+// Bandwidth-bound stages of the NVFP4 Newton-Schulz path on gfx950:
+// p99 clipping threshold (exact radix select), Frobenius normalisation,
+// canonical copies, and the fused rotate + amax / rotate + encode quantiser.
+//
+// Paper: Section 2 ("NVFP4 format", "Root optimizer"), Section 3.4 (p99
+// clipping, NVFP4 NS iteration, RTN + adaptive 4/6), Table 8 (quantile 0.99).
+#include "device.h"
+#include "internal.h"
+
+namespace fp4r {
+
+// ---------------------------------------------------------------------------
+__global__ void k_fill_u32(uint32_t* p, uint32_t v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(k_fill_u32, dim3((uint32_t)blocks), dim3(256), 0, st, p, value, n);
+  return hipGetLastError();
+}
+
+FP4R_DEV int find_matrix(const MatChunk& ch, int64_t tile) {
+  int mi = 0;
+  for (int i = 1; i < ch.count; ++i)
+    if (ch.m[i].tile_begin <= tile) mi = i;
+  return mi;
+}
+
+// ---------------------------------------------------------------------------
+// Clip threshold: tau = fl32(v[lo] + f (v[lo+1] - v[lo])) over the sorted |M|,
+// found with a three-pass radix select on the binary32 bit patterns (31-bit keys,
+// digits of 11, 10 and 10 bits).  Both ranks are tracked in the same passes.
+
+__global__ void k_clip_init(MatChunk ch, MatScalars* sc) {
+  const int i = threadIdx.x;
+  if (i >= ch.count) return;
+  const MatDesc& d = ch.m[i];
+  const int64_t n = d.rows * d.cols;
+  MatScalars& s = sc[i];
+  s.sel_prefix[0] = s.sel_prefix[1] = 0;
+  s.sel_rank[0] = (uint32_t)d.lo;
+  s.sel_rank[1] = (uint32_t)(d.lo + 1 < n ? d.lo + 1 : d.lo);
+}
+
+__global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalars* sc,
+                                                    uint32_t* hist, uint32_t* status, int pass) {
+  __shared__ uint32_t h[2][kHistBins];
+  for (int i = threadIdx.x; i < 2 * kHistBins; i += 256) (&h[0][0])[i] = 0;
+  __syncthreads();
+  const int64_t tile = blockIdx.x;
+  const int mi = find_matrix(ch, tile);
+  const MatDesc& d = ch.m[mi];
+  const int64_t r0 = (tile - d.tile_begin) * kPrepRowsPerBlock;
+  const int64_t r1 = r0 + kPrepRowsPerBlock < d.rows ? r0 + kPrepRowsPerBlock : d.rows;
+  const uint32_t p0 = sc[mi].sel_prefix[0], p1 = sc[mi].sel_prefix[1];
+  const bool two = pass > 0 && p0 != p1;
+  const int pshift = pass == 1 ? 20 : 10;
+  bool bad = false;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float4* row = reinterpret_cast<const float4*>(d.in + r * d.ld_in);
+    for (int64_t c = threadIdx.x; c < d.cols / 4; c += 256) {
+      const float4 v = row[c];
+      const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t key = __float_as_uint(e[j]) & 0x7FFFFFFFu;
+        if (key >= 0x7F800000u) { bad = true; continue; }
+        uint32_t digit;
+        if (pass == 0) {
+          atomicAdd(&h[0][key >> 20], 1u);
+          continue;
+        }
+        digit = pass == 1 ? ((key >> 10) & 1023u) : (key & 1023u);
+        const uint32_t pre = key >> pshift;
+        if (pre == p0) atomicAdd(&h[0][digit], 1u);
+        if (two && pre == p1) atomicAdd(&h[1][digit], 1u);
+      }
+    }
+  }
+  if (bad) atomicOr(status, kStatusNonFinite);
+  __syncthreads();
+  const int nb = pass == 0 ? 2048 : 1024;
+  for (int b = threadIdx.x; b < nb; b += 256) {
+    if (h[0][b]) atomicAdd(&hist[(mi * 2 + 0) * kHistBins + b], h[0][b]);
+    if (two && h[1][b]) atomicAdd(&hist[(mi * 2 + 1) * kHistBins + b], h[1][b]);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_radix_select(MatChunk ch, MatScalars* sc, uint32_t* hist,
+                                                      int pass) {
+  __shared__ uint32_t part[256];
+  __shared__ uint32_t found_prefix[2], found_rank[2];
+  const int mi = blockIdx.x;
+  const int t = threadIdx.x;
+  MatScalars& s = sc[mi];
+  const int nb = pass == 0 ? 2048 : 1024;
+  const int per = nb / 256;
+  const bool two = pass > 0 && s.sel_prefix[0] != s.sel_prefix[1];
+  for (int rr = 0; rr < 2; ++rr) {
+    const uint32_t* hh = hist + (mi * 2 + (two ? rr : 0)) * kHistBins;
+    uint32_t local = 0;
+    for (int j = 0; j < per; ++j) local += hh[t * per + j];
+    part[t] = local;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {   // inclusive Hillis-Steele scan
+      const uint32_t add = t >= off ? part[t - off] : 0u;
+      __syncthreads();
+      part[t] += add;
+      __syncthreads();
+    }
+    const uint32_t incl = part[t];
+    const uint32_t excl = incl - local;
+    const uint32_t target = s.sel_rank[rr];
+    if (target >= excl && target < incl) {   // exactly one thread owns the target rank
+      uint32_t cum = excl;
+      for (int j = 0; j < per; ++j) {
+        const uint32_t c = hh[t * per + j];
+        if (target < cum + c) {
+          const uint32_t bin = (uint32_t)(t * per + j);
+          found_prefix[rr] = pass == 0 ? bin : ((s.sel_prefix[rr] << 10) | bin);
+          found_rank[rr] = target - cum;
+          break;
+        }
+        cum += c;
+      }
+    }
+    __syncthreads();
+  }
+  for (int b = t; b < 2 * kHistBins; b += 256) hist[mi * 2 * kHistBins + b] = 0u;
+  if (t == 0) {
+    s.sel_prefix[0] = found_prefix[0];
+    s.sel_prefix[1] = found_prefix[1];
+    s.sel_rank[0] = found_rank[0];
+    s.sel_rank[1] = found_rank[1];
+    if (pass == 2) {
+      const double v0 = (double)__uint_as_float(found_prefix[0]);
+      const double v1 = (double)__uint_as_float(found_prefix[1]);
+      const double f = ch.m[mi].frac;
+      s.tau = (float)__dadd_rn(v0, __dmul_rn(f, __dsub_rn(v1, v0)));
+    }
+  }
+}
+
+hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* hist,
+                                 uint32_t* status, hipStream_t st) {
+  hipError_t e = launch_fill_u32(hist, 0u, (int64_t)ch.count * 2 * kHistBins, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_clip_init, dim3(1), dim3(kMaxChunk), 0, st, ch, sc);
+  for (int pass = 0; pass < 3; ++pass) {
+    hipLaunchKernelGGL(k_radix_hist, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc,
+                       hist, status, pass);
+    hipLaunchKernelGGL(k_radix_select, dim3(ch.count), dim3(256), 0, st, ch, sc, hist, pass);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Frobenius norm of clamp(M, tau): per-block binary64 partials in a fixed
+// order, then one fixed-order sum per matrix (deterministic).
+
+__global__ __launch_bounds__(256) void k_sumsq(MatChunk ch, const MatScalars* sc, double* partial) {
+  __shared__ double red[256];
+  const int64_t tile = blockIdx.x;
+  const int mi = find_matrix(ch, tile);
+  const MatDesc& d = ch.m[mi];
+  const float tau = sc[mi].tau;
+  const int64_t r0 = (tile - d.tile_begin) * kPrepRowsPerBlock;
+  const int64_t r1 = r0 + kPrepRowsPerBlock < d.rows ? r0 + kPrepRowsPerBlock : d.rows;
+  double acc = 0.0;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float4* row = reinterpret_cast<const float4*>(d.in + r * d.ld_in);
+    for (int64_t c = threadIdx.x; c < d.cols / 4; c += 256) {
+      const float4 v = row[c];
+      const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const double x = (double)fminf(fmaxf(e[j], -tau), tau);
+        acc = acc + x * x;
+      }
+    }
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) partial[tile] = red[0];
+}
+
+__global__ __launch_bounds__(256) void k_norm_final(MatChunk ch, MatScalars* sc, const double* partial,
+                                                    float eps) {
+  __shared__ double red[256];
+  const int mi = blockIdx.x;
+  const MatDesc& d = ch.m[mi];
+  const int64_t nt = (d.rows + kPrepRowsPerBlock - 1) / kPrepRowsPerBlock;
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < nt; i += 256) acc = acc + partial[d.tile_begin + i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double nu = __dsqrt_rn(red[0]);
+    sc[mi].inv_norm = (float)__ddiv_rn(1.0, __dadd_rn(nu, (double)eps));
+  }
+}
+
+hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, float eps,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(k_sumsq, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, partial);
+  hipLaunchKernelGGL(k_norm_final, dim3(ch.count), dim3(256), 0, st, ch, sc, partial, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Tiled copies through LDS (64 x 64 tiles, coalesced on both sides).
+
+constexpr int kT = 64;
+
+FP4R_DEV int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// dir 0 (prep): canonical X = fl32(clamp(M) * inv), transposed when rows > cols.
+// dir 1 (copy-out): M_out = X (transposed back when rows > cols).
+template <int DIR>
+__global__ __launch_bounds__(256) void k_tile_copy(MatChunk ch, const MatScalars* sc, float* xbase,
+                                                   int64_t x_bstride) {
+  __shared__ float tile[kT][kT + 1];
+  const int64_t t = blockIdx.x;
+  const int mi = find_matrix(ch, t);
+  const MatDesc& d = ch.m[mi];
+  const bool tall = d.rows > d.cols;
+  const int64_t tcols = cdiv(d.cols, kT);
+  const int64_t tt = t - d.tile_begin;
+  const int64_t br = (tt / tcols) * kT, bc = (tt % tcols) * kT;  // tile origin in M coordinates
+  float* X = xbase + (int64_t)mi * x_bstride;
+  const int64_t xld = tall ? d.rows : d.cols;   // canonical row length n
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;   // 64 x 4
+  const float tau = DIR == 0 ? sc[mi].tau : 0.0f;
+  const float inv = DIR == 0 ? sc[mi].inv_norm : 0.0f;
+  if (!tall) {
+    for (int i = ty; i < kT; i += 4) {
+      const int64_t r = br + i, c = bc + tx;
+      if (r < d.rows && c < d.cols) {
+        if (DIR == 0) {
+          const float v = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau);
+          X[r * xld + c] = v * inv;
+        } else {
+          d.out[r * d.ld_out + c] = X[r * xld + c];
+        }
+      }
+    }
+    return;
+  }
+  // tall: X[c][r] <-> M[r][c]
+  if (DIR == 0) {
+    for (int i = ty; i < kT; i += 4) {
+      const int64_t r = br + i, c = bc + tx;
+      if (r < d.rows && c < d.cols) tile[i][tx] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
+    }
+    __syncthreads();
+    for (int i = ty; i < kT; i += 4) {
+      const int64_t c = bc + i, r = br + tx;   // X row c, column r
+      if (r < d.rows && c < d.cols) X[c * xld + r] = tile[tx][i];
+    }
+  } else {
+    for (int i = ty; i < kT; i += 4) {
+      const int64_t c = bc + i, r = br + tx;
+      if (r < d.rows && c < d.cols) tile[tx][i] = X[c * xld + r];
+    }
+    __syncthreads();
+    for (int i = ty; i < kT; i += 4) {
+      const int64_t r = br + i, c = bc + tx;
+      if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = tile[i][tx];
+    }
+  }
+}
+
+hipError_t launch_prep_copy(const MatChunk& ch, const MatScalars* sc, float* x, int64_t x_bstride,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(k_tile_copy<0>, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, x,
+                     x_bstride);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride, hipStream_t st) {
+  hipLaunchKernelGGL(k_tile_copy<1>, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch,
+                     (const MatScalars*)nullptr, const_cast<float*>(x), x_bstride);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Quantiser: one thread per 16-element block.  Axis 1: blocks along a row,
+// consecutive threads take consecutive blocks of a row (contiguous 64-byte
+// reads).  Axis 0: blocks down a column, consecutive threads take consecutive
+// columns (each of the 16 loads is a contiguous 256-byte wave access).
+
+template <int AXIS>
+FP4R_DEV bool load_block(const Batch& in, int64_t b, int64_t g, float (&u)[16], int64_t& r, int64_t& c) {
+  const float* x = in.x + b * in.bstride;
+  if (AXIS == 1) {
+    const int64_t nbr = in.cols / 16;
+    r = g / nbr;
+    c = (g % nbr) * 16;
+    const float4* p = reinterpret_cast<const float4*>(x + r * in.ld + c);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = p[q];
+      u[4 * q] = v.x; u[4 * q + 1] = v.y; u[4 * q + 2] = v.z; u[4 * q + 3] = v.w;
+    }
+  } else {
+    c = g % in.cols;
+    r = (g / in.cols) * 16;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) u[i] = x[(r + i) * in.ld + c];
+  }
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ok = ok && ((__float_as_uint(u[i]) & 0x7F800000u) != 0x7F800000u);
+  return ok;
+}
+
+template <int AXIS>
+__global__ __launch_bounds__(256) void k_amax(Batch in, uint32_t mask, int rotate, int clip,
+                                              MatScalars* sc, int slot, uint32_t* status) {
+  __shared__ float red[4];
+  const int64_t b = blockIdx.y;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nblk = in.rows * in.cols / 16;
+  float m = 0.0f;
+  if (g < nblk) {
+    float u[16];
+    int64_t r, c;
+    const bool ok = load_block<AXIS>(in, b, g, u, r, c);
+    if (!ok) atomicOr(status, kStatusNonFinite);
+    if (clip) {
+      const float tau = sc[b].tau;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
+    }
+    if (rotate) rotate16(u, mask);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(u[i]));
+    if (!ok) m = 0.0f;
+  }
+  m = warp_max(m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float mm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    atomicMax(&sc[b].amax[slot], __float_as_uint(mm));
+  }
+}
+
+template <int AXIS>
+__global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rotate, int clip,
+                                                int adaptive, MatScalars* sc, int slot, QOut out,
+                                                float* tensor_scale) {
+  const int64_t b = blockIdx.y;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nblk = in.rows * in.cols / 16;
+  const float sg = tensor_scale_from_amax(sc[b].amax[slot]);
+  if (g == 0) {
+    sc[b].sg[slot] = sg;
+    if (tensor_scale) tensor_scale[b] = sg;
+  }
+  if (g >= nblk) return;
+  float u[16];
+  int64_t r, c;
+  load_block<AXIS>(in, b, g, u, r, c);
+  if (clip) {
+    const float tau = sc[b].tau;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
+  }
+  if (rotate) rotate16(u, mask);
+  uint32_t scale;
+  uint64_t codes;
+  quant_block(u, sg, adaptive != 0, scale, codes);
+  int64_t code_off, scale_off;
+  if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
+    code_off = r * (in.cols / 2) + c / 2;
+    scale_off = r * (in.cols / 16) + c / 16;
+  } else {           // transposed: [cols][rows/2], [cols][rows/16]
+    code_off = c * (in.rows / 2) + r / 2;
+    scale_off = c * (in.rows / 16) + r / 16;
+  }
+  *reinterpret_cast<uint2*>(out.codes + b * out.codes_bstride + code_off) =
+      make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+  out.scales[b * out.scales_bstride + scale_off] = (uint8_t)scale;
+}
+
+hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
+                       MatScalars* sc, int slot, uint32_t* status, hipStream_t st) {
+  const int64_t nblk = in.rows * in.cols / 16;
+  const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
+  if (axis == 1)
+    hipLaunchKernelGGL(k_amax<1>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip, sc,
+                       slot, status);
+  else
+    hipLaunchKernelGGL(k_amax<0>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip, sc,
+                       slot, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
+                         bool adaptive46, MatScalars* sc, int slot, const QOut& out,
+                         float* tensor_scale, hipStream_t st) {
+  const int64_t nblk = in.rows * in.cols / 16;
+  const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
+  if (axis == 1)
+    hipLaunchKernelGGL(k_encode<1>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
+                       (int)adaptive46, sc, slot, out, tensor_scale);
+  else
+    hipLaunchKernelGGL(k_encode<0>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
+                       (int)adaptive46, sc, slot, out, tensor_scale);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// BF16 comparison path: Xb = bf16(X) and Xbt = bf16(X)^T (round to nearest even).
+
+FP4R_DEV uint16_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__global__ __launch_bounds__(256) void k_cast_bf16(const float* x, int64_t m, int64_t n,
+                                                   int64_t x_bstride, uint16_t* xb, uint16_t* xbt,
+                                                   int64_t b_bstride) {
+  __shared__ uint16_t tile[kT][kT + 2];
+  const int64_t b = blockIdx.y;
+  const int64_t tn = cdiv(n, kT);
+  const int64_t br = (blockIdx.x / tn) * kT, bc = (blockIdx.x % tn) * kT;
+  const float* X = x + b * x_bstride;
+  uint16_t* Xb = xb + b * b_bstride;
+  uint16_t* Xt = xbt + b * b_bstride;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < kT; i += 4) {
+    const int64_t r = br + i, c = bc + tx;
+    if (r < m && c < n) {
+      const uint16_t h = bf16_rne(X[r * n + c]);
+      Xb[r * n + c] = h;
+      tile[i][tx] = h;
+    }
+  }
+  __syncthreads();
+  for (int i = ty; i < kT; i += 4) {
+    const int64_t c = bc + i, r = br + tx;
+    if (r < m && c < n) Xt[c * m + r] = tile[tx][i];
+  }
+}
+
+hipError_t launch_cast_bf16(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
+                            uint16_t* xb, uint16_t* xbt, int64_t b_bstride, hipStream_t st) {
+  const dim3 grid((uint32_t)(((m + kT - 1) / kT) * ((n + kT - 1) / kT)), (uint32_t)batch);
+  hipLaunchKernelGGL(k_cast_bf16, grid, dim3(256), 0, st, x, m, n, x_bstride, xb, xbt, b_bstride);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Small per-matrix scalar kernels.
+
+__global__ void k_reset_scalars(MatScalars* sc, int64_t n, int full) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  MatScalars& s = sc[i];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) s.amax[k] = 0u;
+  if (full) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s.sg[k] = 0.0f;
+    s.tau = __uint_as_float(0x7F800000u);   // +inf: clamping is the identity
+    s.inv_norm = 1.0f;
+  }
+}
+
+hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, bool full, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_reset_scalars, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, st, sc, n,
+                     (int)full);
+  return hipGetLastError();
+}
+
+__global__ void k_export_scalar(const MatScalars* sc, int64_t n, int which, int slot, float* out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  out[i] = which == 0 ? sc[i].tau : sc[i].sg[slot];
+}
+
+hipError_t launch_export_scalar(const MatScalars* sc, int64_t n, int which, int slot, float* out,
+                                hipStream_t st) {
+  if (n <= 0 || !out) return hipSuccess;
+  hipLaunchKernelGGL(k_export_scalar, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, st, sc, n,
+                     which, slot, out);
+  return hipGetLastError();
+}
+
+}  // namespace fp4r

@@ -1,0 +1,289 @@
+"""ctypes binding of libfp4root.so (argument marshalling only).
+
+Every function here checks its tensors, passes raw device pointers, sizes and
+the current HIP stream to the C entry point of the same name, and raises
+``Fp4RootError`` on a non-zero return code.  Device memory for outputs and the
+workspace comes from PyTorch; all computation happens in the library's
+kernels.  There is no CPU path: without the built library or a GPU every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfp4root.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "fp4root.h")
+
+OK = 0
+F_CLIP = 1
+F_HADAMARD = 2
+F_ADAPTIVE46 = 4
+F_BF16_PATH = 8
+F_DEFAULT = 7
+
+
+class Fp4RootError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} ({code})")
+
+
+class Matrix(ctypes.Structure):
+    _fields_ = [("in_", ctypes.c_void_p), ("out", ctypes.c_void_p), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int64), ("ld_in", ctypes.c_int64), ("ld_out", ctypes.c_int64)]
+
+
+class NsConfig(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int32), ("coeffs", ctypes.POINTER(ctypes.c_float)),
+                ("flags", ctypes.c_uint32), ("clip_quantile", ctypes.c_float),
+                ("eps", ctypes.c_float), ("seed", ctypes.c_uint64)]
+
+
+class NsTrace(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in (
+        "qx_codes", "qx_scales", "qx_sg", "qxt_codes", "qxt_scales", "qxt_sg", "A",
+        "qa_codes", "qa_scales", "qa_sg", "B", "qb_codes", "qb_scales", "qb_sg")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libfp4root.so not built at {path}; run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    i64, u32, u64, f32, vp, i32 = (ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64,
+                                   ctypes.c_float, ctypes.c_void_p, ctypes.c_int32)
+    sz = ctypes.c_size_t
+    lib.fp4root_quantize_workspace.argtypes = [i64, i64, i64, u32]
+    lib.fp4root_quantize_workspace.restype = sz
+    lib.fp4root_ns_step_workspace.argtypes = [i64, i64, i64, u32]
+    lib.fp4root_ns_step_workspace.restype = sz
+    lib.fp4root_orthogonalize_workspace.argtypes = [ctypes.POINTER(Matrix), i64, ctypes.POINTER(NsConfig)]
+    lib.fp4root_orthogonalize_workspace.restype = sz
+    lib.fp4root_quantize.argtypes = [vp, i64, i64, i64, i64, i64, ctypes.c_int, u32, f32, u64, i32,
+                                     vp, vp, vp, vp, vp, sz, vp]
+    lib.fp4root_quantize.restype = ctypes.c_int
+    lib.fp4root_ns_step.argtypes = [vp, i64, i64, i64, i64, f32, f32, f32, u32, u64, i32,
+                                    ctypes.POINTER(NsTrace), vp, sz, vp]
+    lib.fp4root_ns_step.restype = ctypes.c_int
+    lib.fp4root_orthogonalize.argtypes = [ctypes.POINTER(Matrix), i64, ctypes.POINTER(NsConfig), vp, sz, vp]
+    lib.fp4root_orthogonalize.restype = ctypes.c_int
+    lib.fp4root_default_coeffs.argtypes = [i64, i64, i32, ctypes.POINTER(ctypes.c_float)]
+    lib.fp4root_default_coeffs.restype = ctypes.c_int
+    lib.fp4root_device_status.argtypes = [vp, vp]
+    lib.fp4root_device_status.restype = ctypes.c_int
+    lib.fp4root_status_string.argtypes = [ctypes.c_int]
+    lib.fp4root_status_string.restype = ctypes.c_char_p
+    lib.fp4root_version.argtypes = []
+    lib.fp4root_version.restype = ctypes.c_int
+    lib.fp4root_timer_enable.argtypes = [ctypes.c_int]
+    lib.fp4root_timer_enable.restype = ctypes.c_int
+    lib.fp4root_timer_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)]
+    lib.fp4root_timer_read.restype = ctypes.c_int
+    lib.fp4root_timer_reset.argtypes = []
+    lib.fp4root_timer_reset.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def header_symbols(path: str = HEADER) -> list[str]:
+    """Names of the functions include/fp4root.h declares."""
+    text = open(path).read()
+    return sorted(set(re.findall(r"^\s*(?:const char\*|int|size_t)\s+(fp4root_\w+)\s*\(", text, re.M)))
+
+
+def status_string(code: int) -> str:
+    return load().fp4root_status_string(code).decode()
+
+
+def _check(code: int, where: str):
+    if code != OK:
+        raise Fp4RootError(code, where)
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _need_gpu_f32(x: torch.Tensor, name: str):
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if x.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def fp4root_version() -> int:
+    return load().fp4root_version()
+
+
+def fp4root_timer_enable(on: bool = True):
+    _check(load().fp4root_timer_enable(1 if on else 0), "fp4root_timer_enable")
+
+
+def fp4root_timer_read(kernel: int = -1):
+    """(total kernel ms, launches, algorithmic FLOP) of the recorded product launches."""
+    ms, n, fl = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
+    _check(load().fp4root_timer_read(kernel, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl)),
+           "fp4root_timer_read")
+    return ms.value, n.value, fl.value
+
+
+def fp4root_timer_reset():
+    _check(load().fp4root_timer_reset(), "fp4root_timer_reset")
+
+
+def fp4root_default_coeffs(rows: int, cols: int, steps: int = 5):
+    buf = (ctypes.c_float * (3 * steps))()
+    _check(load().fp4root_default_coeffs(rows, cols, steps, buf), "fp4root_default_coeffs")
+    return [(buf[3 * k], buf[3 * k + 1], buf[3 * k + 2]) for k in range(steps)]
+
+
+def fp4root_device_status(ws: torch.Tensor, stream=None) -> int:
+    return load().fp4root_device_status(_ptr(ws), _stream(stream))
+
+
+def fp4root_quantize(x: torch.Tensor, axis: int = 1, flags: int = F_HADAMARD | F_ADAPTIVE46,
+                     clip_quantile: float = 0.99, seed: int = 0, step: int = 0, ws=None, stream=None):
+    """NVFP4-quantise a matrix or a batch (B, rows, cols) of float32 matrices.
+
+    Returns (codes, scales, tensor_scale, clip_threshold, ws); codes hold two
+    4-bit codes per byte.  See fp4root_quantize in include/fp4root.h.
+    """
+    _need_gpu_f32(x, "x")
+    lib = load()
+    xb = x if x.dim() == 3 else x.unsqueeze(0)
+    if xb.stride(-1) != 1:
+        raise ValueError("x rows must be contiguous")
+    B, R, C = xb.shape
+    ld = xb.stride(1)
+    bstride = xb.stride(0) if B > 1 else R * ld
+    dev = x.device
+    if axis == 1:
+        codes = torch.empty((B, R, C // 2), dtype=torch.uint8, device=dev)
+        scales = torch.empty((B, R, C // 16), dtype=torch.uint8, device=dev)
+    else:
+        codes = torch.empty((B, C, R // 2), dtype=torch.uint8, device=dev)
+        scales = torch.empty((B, C, R // 16), dtype=torch.uint8, device=dev)
+    sg = torch.empty(B, dtype=torch.float32, device=dev)
+    tau = torch.empty(B, dtype=torch.float32, device=dev)
+    need = lib.fp4root_quantize_workspace(B, R, C, flags)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check(lib.fp4root_quantize(_ptr(xb), B, R, C, ld, bstride, axis, flags, clip_quantile, seed,
+                                step, _ptr(codes), _ptr(scales), _ptr(sg), _ptr(tau), _ptr(ws),
+                                ws.numel(), _stream(stream)), "fp4root_quantize")
+    if x.dim() == 2:
+        codes, scales = codes[0], scales[0]
+    return codes, scales, sg, tau, ws
+
+
+def fp4root_ns_step(x: torch.Tensor, a: float, b: float, c: float,
+                    flags: int = F_HADAMARD | F_ADAPTIVE46, seed: int = 0, step: int = 0,
+                    trace: bool = False, ws=None, stream=None):
+    """One NS step in place on x (m, n) or (B, m, n).  With trace=True returns a dict of
+    the step's intermediates (qX, qXt, A, qA, B, qB), else None."""
+    _need_gpu_f32(x, "x")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    lib = load()
+    xb = x if x.dim() == 3 else x.unsqueeze(0)
+    B, m, n = xb.shape
+    need = lib.fp4root_ns_step_workspace(B, m, n, flags)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, x.device)
+    tr = None
+    out = None
+    if trace:
+        dev = x.device
+        u8 = dict(dtype=torch.uint8, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        out = {
+            "qx_codes": torch.empty((B, m, n // 2), **u8), "qx_scales": torch.empty((B, m, n // 16), **u8),
+            "qx_sg": torch.empty(B, **f32),
+            "qxt_codes": torch.empty((B, n, m // 2), **u8), "qxt_scales": torch.empty((B, n, m // 16), **u8),
+            "qxt_sg": torch.empty(B, **f32),
+            "A": torch.empty((B, m, m), **f32),
+            "qa_codes": torch.empty((B, m, m // 2), **u8), "qa_scales": torch.empty((B, m, m // 16), **u8),
+            "qa_sg": torch.empty(B, **f32),
+            "B": torch.empty((B, m, m), **f32),
+            "qb_codes": torch.empty((B, m, m // 2), **u8), "qb_scales": torch.empty((B, m, m // 16), **u8),
+            "qb_sg": torch.empty(B, **f32),
+        }
+        tr = NsTrace(**{k: v.data_ptr() for k, v in out.items()})
+    _check(lib.fp4root_ns_step(_ptr(xb), B, m, n, m * n, a, b, c, flags, seed, step,
+                               ctypes.byref(tr) if tr is not None else None, _ptr(ws), ws.numel(),
+                               _stream(stream)), "fp4root_ns_step")
+    return out
+
+
+class Orthogonalizer:
+    """Reusable call of fp4root_orthogonalize over a fixed list of matrices.
+
+    Holds the descriptor array, the configuration and the workspace so that a
+    timed loop makes exactly one C call per invocation.
+    """
+
+    def __init__(self, inputs, outputs=None, steps: int = 5, coeffs=None, flags: int = F_DEFAULT,
+                 clip_quantile: float = 0.99, eps: float = 1e-7, seed: int = 0):
+        lib = load()
+        self.inputs = list(inputs)
+        self.outputs = list(outputs) if outputs is not None else [torch.empty_like(t) for t in self.inputs]
+        n = len(self.inputs)
+        self.mats = (Matrix * max(n, 1))()
+        for i, (a, o) in enumerate(zip(self.inputs, self.outputs)):
+            _need_gpu_f32(a, f"inputs[{i}]")
+            _need_gpu_f32(o, f"outputs[{i}]")
+            if a.dim() != 2 or a.stride(1) != 1 or o.stride(1) != 1 or o.shape != a.shape:
+                raise ValueError(f"matrix {i}: need 2-D row-contiguous input and output of equal shape")
+            self.mats[i] = Matrix(a.data_ptr(), o.data_ptr(), a.shape[0], a.shape[1], a.stride(0), o.stride(0))
+        self.count = n
+        if coeffs is not None:
+            flat = [float(v) for row in coeffs for v in row]
+            if len(flat) != 3 * steps:
+                raise ValueError("coeffs must hold steps rows of (a, b, c)")
+            self._coeffs = (ctypes.c_float * len(flat))(*flat)
+            cptr = ctypes.cast(self._coeffs, ctypes.POINTER(ctypes.c_float))
+        else:
+            self._coeffs = None
+            cptr = None
+        self.cfg = NsConfig(steps, cptr, flags, clip_quantile, eps, seed)
+        need = lib.fp4root_orthogonalize_workspace(self.mats, n, ctypes.byref(self.cfg))
+        if need == 0:
+            raise ValueError("invalid matrices or configuration")
+        dev = self.inputs[0].device if n else torch.device("cuda")
+        self.ws = workspace(need, dev)
+
+    def __call__(self, stream=None):
+        _check(load().fp4root_orthogonalize(self.mats, self.count, ctypes.byref(self.cfg),
+                                            _ptr(self.ws), self.ws.numel(), _stream(stream)),
+               "fp4root_orthogonalize")
+        return self.outputs
+
+    def status(self, stream=None) -> int:
+        return fp4root_device_status(self.ws, stream)
+
+
+def fp4root_orthogonalize(inputs, outputs=None, steps: int = 5, coeffs=None, flags: int = F_DEFAULT,
+                          clip_quantile: float = 0.99, eps: float = 1e-7, seed: int = 0, stream=None):
+    """Orthogonalise a list of float32 GPU matrices; returns the outputs (new tensors unless given)."""
+    return Orthogonalizer(inputs, outputs, steps, coeffs, flags, clip_quantile, eps, seed)(stream)

@@ -1,0 +1,152 @@
+"""GPU parity of the Newton-Schulz path against the oracle.
+
+Each stage of a step is checked against the oracle fed with the GPU's own
+previous stage (quantisations bit for bit, products to the binary32 value),
+then whole orthogonalisations end to end within the 1e-3 relative Frobenius
+tolerance (the products are exact, so the observed error is expected to be 0).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ns, rht
+from oracle.ns import gram64
+from oracle.quantize import quantize
+from paper_2607_04422_amd import workloads
+from tests.gpu_util import assert_same_nvfp4, gpu_nvfp4, need_gpu, np_, rel_fro, ulp_diff
+
+pytestmark = pytest.mark.gpu
+
+F = None
+TOL = 1e-3
+# BF16 comparison path: products accumulate in binary32 before their bf16 rounding,
+# so about one element in 2^14 rounds to the neighbouring bf16 value (a 2^-8
+# relative change of that element); through five steps these flips move the output
+# by up to about 2^-8 relative.  Tolerance: 2^-7.
+TOL_BF16 = 2.0 ** -7
+CONV = [(1.875, -1.25, 0.375)] * 5
+MIXED = [(3.0, -3.2, 1.2)] * 3 + [(1.875, -1.25, 0.375)] * 2
+
+
+def setup_module():
+    global F
+    need_gpu()
+    from paper_2607_04422_amd import fp4root
+    F = fp4root
+
+
+def _check_step(x0, a, b, c, flags, seed, step, tr, x1):
+    """Stage-by-stage comparison of one traced GPU step with the oracle."""
+    signs = rht.step_signs(seed, step) if flags & F.F_HADAMARD else None
+    ad = bool(flags & F.F_ADAPTIVE46)
+    qx = gpu_nvfp4(tr["qx_codes"][0], tr["qx_scales"][0], tr["qx_sg"])
+    qxt = gpu_nvfp4(tr["qxt_codes"][0], tr["qxt_scales"][0], tr["qxt_sg"])
+    assert_same_nvfp4(qx, quantize(x0, 1, signs, ad), "qX")
+    assert_same_nvfp4(qxt, quantize(x0, 0, signs, ad), "qXt")
+    A = np_(tr["A"][0])
+    A_ref = ns.f32((np.float64(qx.sg) ** 2) * gram64(qx.block_values()))
+    assert np.array_equal(A, A.T)
+    assert ulp_diff(A, A_ref).max() <= 1 and np.count_nonzero(A != A_ref) <= max(2, A.size // 10**6)
+    qa = gpu_nvfp4(tr["qa_codes"][0], tr["qa_scales"][0], tr["qa_sg"])
+    assert_same_nvfp4(qa, quantize(A, 1, signs, ad), "qA")
+    B = np_(tr["B"][0])
+    P = (np.float64(qa.sg) ** 2) * gram64(qa.block_values())
+    B_ref = ns.f32(np.float64(np.float32(b)) * A.astype(np.float64) + np.float64(np.float32(c)) * P)
+    assert np.array_equal(B, B.T)
+    assert ulp_diff(B, B_ref).max() <= 1 and np.count_nonzero(B != B_ref) <= max(2, B.size // 10**6)
+    qb = gpu_nvfp4(tr["qb_codes"][0], tr["qb_scales"][0], tr["qb_sg"])
+    assert_same_nvfp4(qb, quantize(B, 1, signs, ad), "qB")
+    prod = qb.block_values() @ qxt.block_values().T
+    X_ref = ns.f32(np.float64(np.float32(a)) * x0.astype(np.float64)
+                   + np.float64(qb.sg) * np.float64(qxt.sg) * prod)
+    assert ulp_diff(x1, X_ref).max() <= 1 and np.count_nonzero(x1 != X_ref) <= max(2, x1.size // 10**6)
+
+
+@pytest.mark.parametrize("shape", [(64, 128), (256, 512), (272, 400), (144, 144), (272, 144)])
+@pytest.mark.parametrize("flags", [6, 0])
+def test_ns_step_stages(shape, flags):
+    m, n = shape
+    x0, _, _ = ns.prepare(workloads.matrix(m, n, seed=m + n, kind="t_rows"))
+    if x0.shape != (m, n):
+        x0 = np.ascontiguousarray(x0.T)
+    a, b, c = MIXED[0]
+    x = torch.from_numpy(x0).cuda()
+    tr = F.fp4root_ns_step(x, a, b, c, flags=flags, seed=77, step=2, trace=True)
+    _check_step(x0, a, b, c, flags, 77, 2, tr, np_(x))
+    # the untraced call produces the same bits
+    y = torch.from_numpy(x0).cuda()
+    F.fp4root_ns_step(y, a, b, c, flags=flags, seed=77, step=2)
+    assert torch.equal(x, y)
+
+
+def test_ns_step_matches_oracle_step():
+    x0, _, _ = ns.prepare(workloads.matrix(256, 768, seed=4))
+    x = torch.from_numpy(x0).cuda()
+    for k, (a, b, c) in enumerate(MIXED):
+        ref = ns.ns_step_nvfp4(np_(x), a, b, c, rht.step_signs(5, k), True)
+        F.fp4root_ns_step(x, a, b, c, flags=6, seed=5, step=k)
+        assert rel_fro(np_(x), ref) <= TOL
+        assert np.count_nonzero(np_(x) != ref) <= 2
+
+
+def _orth_case(mats, coeffs, flags, seed=0, mode="nvfp4"):
+    ins = [torch.from_numpy(m).cuda() for m in mats]
+    orth = F.Orthogonalizer(ins, steps=len(coeffs), coeffs=coeffs, flags=flags, seed=seed)
+    outs = orth()
+    assert orth.status() == 0
+    errs = []
+    for m, o in zip(mats, outs):
+        ref = ns.orthogonalize(m, coeffs, clip_on=bool(flags & F.F_CLIP), hadamard=bool(flags & F.F_HADAMARD),
+                               adaptive46=bool(flags & F.F_ADAPTIVE46), seed=seed, mode=mode)
+        errs.append(rel_fro(np_(o), ref))
+    return errs
+
+
+def test_orthogonalize_small_case():
+    mats = workloads.small_case()
+    errs = _orth_case(mats, MIXED, F.F_DEFAULT, seed=3)
+    assert max(errs) <= TOL, errs
+
+
+@pytest.mark.parametrize("flags", [7, 6, 1, 0])
+def test_orthogonalize_mixed_shapes(flags):
+    # wide, tall, square and ragged shapes in one call; equal canonical shapes are batched
+    shapes = [(128, 256), (256, 128), (144, 144), (96, 400), (400, 96), (128, 256)]
+    mats = [workloads.matrix(r, c, seed=10 + i, kind="normal_outliers") for i, (r, c) in enumerate(shapes)]
+    errs = _orth_case(mats, MIXED, flags, seed=11)
+    assert max(errs) <= TOL, errs
+
+
+def test_orthogonalize_bf16_path():
+    mats = [workloads.matrix(256, 512, seed=1), workloads.matrix(384, 128, seed=2)]
+    errs = _orth_case(mats, MIXED, F.F_CLIP | F.F_BF16_PATH, mode="bf16")
+    assert max(errs) <= TOL_BF16, errs
+
+
+def test_orthogonalize_default_coeffs_and_zero_steps():
+    m = workloads.matrix(128, 384, seed=21)
+    x = torch.from_numpy(m).cuda()
+    out0 = F.fp4root_orthogonalize([x], steps=0)[0]
+    x_ref, _, _ = ns.prepare(m)
+    assert np.array_equal(np_(out0), x_ref)
+    co = F.fp4root_default_coeffs(128, 384, 5)
+    out = F.fp4root_orthogonalize([x], steps=5)[0]
+    ref = ns.orthogonalize(m, co, seed=0)
+    assert rel_fro(np_(out), ref) <= TOL
+
+
+def test_in_place_and_determinism():
+    m = workloads.matrix(256, 512, seed=31)
+    x1 = torch.from_numpy(m).cuda()
+    out1 = F.fp4root_orthogonalize([x1], steps=5, coeffs=MIXED)[0]
+    x2 = torch.from_numpy(m).cuda()
+    F.fp4root_orthogonalize([x2], outputs=[x2], steps=5, coeffs=MIXED)
+    assert torch.equal(out1, x2)
+
+
+def test_nonfinite_input_reported():
+    m = workloads.matrix(64, 128, seed=1)
+    m[3, 3] = np.nan
+    orth = F.Orthogonalizer([torch.from_numpy(m).cuda()], steps=1, coeffs=MIXED[:1])
+    orth()
+    assert orth.status() == -4

@@ -1,0 +1,102 @@
+"""GPU parity: the HIP quantiser against the oracle, bit for bit (codes, E4M3 scales, FP32 s_g)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import rht
+from oracle.quantile import clip, clip_threshold
+from oracle.quantize import quantize
+from paper_2607_04422_amd import workloads
+from tests.gpu_util import assert_same_nvfp4, gpu_nvfp4, need_gpu, np_
+
+pytestmark = pytest.mark.gpu
+
+F = None
+
+
+def setup_module():
+    global F
+    need_gpu()
+    from paper_2607_04422_amd import fp4root
+    F = fp4root
+
+
+SHAPES = [(16, 16), (48, 80), (256, 512), (272, 400), (1024, 3072)]
+FLAGS = [0, 2, 4, 6, 7]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("flags", FLAGS)
+@pytest.mark.parametrize("axis", [1, 0])
+def test_quantize_parity(shape, flags, axis):
+    r, c = shape
+    m = workloads.matrix(r, c, seed=r * 7 + c, kind="t_rows")
+    seed, step = 1234 + flags, 3
+    x = torch.from_numpy(m).cuda()
+    codes, scales, sg, tau, ws = F.fp4root_quantize(x, axis=axis, flags=flags, clip_quantile=0.99,
+                                                    seed=seed, step=step)
+    assert F.fp4root_device_status(ws) == 0
+    src = m
+    if flags & F.F_CLIP:
+        t = clip_threshold(m, 0.99)
+        assert np_(tau)[0] == t, f"clip threshold {np_(tau)[0]!r} != {t!r}"
+        src = clip(m, t)
+    signs = rht.step_signs(seed, step) if flags & F.F_HADAMARD else None
+    ref = quantize(src, axis, signs, bool(flags & F.F_ADAPTIVE46))
+    assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"{shape} axis={axis} flags={flags}")
+
+
+def test_quantize_batch_and_strides():
+    rng = np.random.default_rng(3)
+    big = rng.standard_normal((3, 64, 160)).astype(np.float32)
+    x = torch.from_numpy(big).cuda()[:, :, :128]       # row stride 160, batch stride 64*160
+    codes, scales, sg, tau, _ = F.fp4root_quantize(x, axis=1, flags=7, seed=9)
+    for b in range(3):
+        src = clip(big[b, :, :128], clip_threshold(big[b, :, :128], 0.99))
+        ref = quantize(src, 1, rht.step_signs(9, 0), True)
+        assert_same_nvfp4(gpu_nvfp4(codes[b], scales[b], sg[b:b + 1]), ref, f"batch {b}")
+
+
+def test_quantize_edge_cases():
+    z = np.zeros((32, 64), np.float32)
+    x = torch.from_numpy(z).cuda()
+    for flags in (0, 6):
+        codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=1, flags=flags)
+        assert np_(sg)[0] == 0 and not np_(scales).any()
+        # a rotated zero block holds -0.0 where a sign was flipped: the sign bit is kept
+        ref = quantize(z, 1, rht.step_signs(0, 0) if flags & 2 else None, bool(flags & 4))
+        assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"zeros flags={flags}")
+    m = np.zeros((32, 64), np.float32)
+    m[3, 17] = -2.5e-30     # tiny single value: subnormal-range scale arithmetic
+    m[20, 40] = 1e-38
+    x = torch.from_numpy(m).cuda()
+    for flags in (0, 6):
+        codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=1, flags=flags)
+        ref = quantize(m, 1, rht.step_signs(0, 0) if flags & 2 else None, bool(flags & 4))
+        assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"tiny flags={flags}")
+
+
+def test_quantize_nonfinite_reported():
+    m = np.ones((32, 32), np.float32)
+    m[5, 7] = np.inf
+    x = torch.from_numpy(m).cuda()
+    _, _, _, _, ws = F.fp4root_quantize(x, axis=1, flags=6)
+    assert F.fp4root_device_status(ws) == -4
+    m[5, 7] = np.nan
+    x = torch.from_numpy(m).cuda()
+    _, _, _, _, ws = F.fp4root_quantize(x, axis=0, flags=7)
+    assert F.fp4root_device_status(ws) == -4
+
+
+def test_quantize_full_size_sampled_rows():
+    """3072 x 8192 (a 3B-shaped MLP matrix): full GPU quantisation, oracle on sampled rows."""
+    m = workloads.matrix(3072, 8192, seed=11, kind="t_rows")
+    x = torch.from_numpy(m).cuda()
+    rng = np.random.default_rng(0)
+    for axis in (1, 0):
+        codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=axis, flags=6, seed=5, step=1)
+        nrows = m.shape[0] if axis == 1 else m.shape[1]
+        sel = np.sort(rng.choice(nrows, 48, replace=False))
+        ref = quantize(m, axis, rht.step_signs(5, 1), True, rows=sel)
+        got = gpu_nvfp4(codes[sel], scales[sel], sg)
+        assert_same_nvfp4(got, ref, f"full-size axis={axis}")

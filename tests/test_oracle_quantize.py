@@ -177,3 +177,15 @@ def test_rejects_non_finite():
     x[0, 4] = np.nan
     with pytest.raises(ValueError):
         quantize(x, 1)
+
+
+@pytest.mark.parametrize("axis", [0, 1])
+def test_row_subset_equals_full(axis):
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((64, 96)).astype(np.float32)
+    d = rht.step_signs(2, 4)
+    full = quantize(x, axis, d)
+    sel = np.array([0, 5, 17, 40])
+    part = quantize(x, axis, d, rows=sel)
+    assert part.sg == full.sg
+    assert np.array_equal(part.codes, full.codes[sel]) and np.array_equal(part.scales, full.scales[sel])
