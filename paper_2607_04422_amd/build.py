@@ -18,6 +18,8 @@ HIPCC_FLAGS = [
     # never emit packed FP32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
+    # MFMA results in VGPRs: the exact product reads every result on the VALU
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
 
 
@@ -28,16 +30,16 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, jobs: int = 3) -> str:
-    """Compile every source for gfx950 and link libfp4root.so; returns its path."""
-    objdir = os.path.join(HERE, "_build")
+def build(verbose: bool = False, jobs: int = 3, extra_flags=(), out: str = LIB) -> str:
+    """Compile every source for gfx950 and link the library (default libfp4root.so); returns its path."""
+    objdir = os.path.join(HERE, "_build", os.path.basename(out) + ".d")
     os.makedirs(objdir, exist_ok=True)
     cc = hipcc()
     procs, objs = [], []
     for src in SOURCES:
         obj = os.path.join(objdir, src + ".o")
         objs.append(obj)
-        cmd = [cc, *HIPCC_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [cc, *HIPCC_FLAGS, *extra_flags, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
@@ -45,15 +47,15 @@ def build(verbose: bool = False, jobs: int = 3) -> str:
             _wait(procs.pop(0))
     while procs:
         _wait(procs.pop(0))
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     cmd = [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
-    out = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
-    if out.returncode != 0:
-        raise RuntimeError("link failed:\n" + out.stdout)
-    os.replace(tmp, LIB)
-    return LIB
+    res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("link failed:\n" + res.stdout)
+    os.replace(tmp, out)
+    return out
 
 
 def _wait(item):

@@ -62,17 +62,52 @@ FP4R_DEV float e4m3_value(uint32_t c) {
   return __uint_as_float(((e + 120u) << 23) | (m << 20));
 }
 
-// E2M1 magnitude index of y in [0, 6]: the number of grid midpoints below y,
-// a tie at a midpoint resolved towards the even index.
-FP4R_DEV uint32_t e2m1_index(float y) {
-  return (uint32_t)(y > 0.25f) + (uint32_t)(y >= 0.75f) + (uint32_t)(y > 1.25f) +
-         (uint32_t)(y >= 1.75f) + (uint32_t)(y > 2.5f) + (uint32_t)(y >= 3.5f) +
-         (uint32_t)(y > 5.0f);
+// Binary32 rounding of a positive binary64 value downwards / upwards.
+FP4R_DEV float rd32(double x) {
+  float f = (float)x;
+  if ((double)f > x) f = __uint_as_float(__float_as_uint(f) - 1u);
+  return f;
+}
+FP4R_DEV float ru32(double x) {
+  float f = (float)x;
+  if ((double)f < x) f = __uint_as_float(__float_as_uint(f) + 1u);
+  return f;
 }
 
-FP4R_DEV double e2m1_value64(uint32_t idx) {
-  // 0, 0.5, 1, 1.5 = idx/2 for idx < 4; 2, 3, 4, 6 above.
-  return idx < 4 ? 0.5 * (double)idx : (idx == 7 ? 6.0 : (double)(idx - 2));
+// E2M1 magnitude index of fl32(a / r) for a >= 0, r > 0, without dividing.
+// The index counts the grid midpoints t crossed by y = fl32(a / r): y > t for
+// t in {0.25, 1.25, 2.5, 5} and y >= t for t in {0.75, 1.75, 3.5} (ties to the
+// even index).  Every t has an even binary32 significand, so y > t exactly when
+// the quotient exceeds the binary32 midpoint t + ulp(t)/2, and y >= t exactly
+// when it reaches the midpoint t - ulp(t^-)/2 below t.  Those midpoints have 25
+// significant bits, so midpoint * r is exact in binary64, and for a binary32 a:
+// a > X  <=>  a > RD32(X),  a >= X  <=>  a >= RU32(X).
+struct E2m1Thresholds {
+  float t[7];
+};
+
+FP4R_DEV E2m1Thresholds e2m1_thresholds(float r) {
+  const double rd = (double)r;
+  E2m1Thresholds th;
+  th.t[0] = rd32((0.25 + 0x1p-26) * rd);
+  th.t[1] = ru32((0.75 - 0x1p-25) * rd);
+  th.t[2] = rd32((1.25 + 0x1p-24) * rd);
+  th.t[3] = ru32((1.75 - 0x1p-24) * rd);
+  th.t[4] = rd32((2.5 + 0x1p-23) * rd);
+  th.t[5] = ru32((3.5 - 0x1p-23) * rd);
+  th.t[6] = rd32((5.0 + 0x1p-22) * rd);
+  return th;
+}
+
+FP4R_DEV uint32_t e2m1_index_thr(float a, const E2m1Thresholds& th) {
+  return (uint32_t)(a > th.t[0]) + (uint32_t)(a >= th.t[1]) + (uint32_t)(a > th.t[2]) +
+         (uint32_t)(a >= th.t[3]) + (uint32_t)(a > th.t[4]) + (uint32_t)(a >= th.t[5]) +
+         (uint32_t)(a > th.t[6]);
+}
+
+// Twice the E2M1 magnitude of an index: {0, 1, 2, 3, 4, 6, 8, 12}.
+FP4R_DEV uint32_t e2m1_twice(uint32_t idx) {
+  return idx < 4 ? idx : ((2u + (idx & 1u)) << ((idx >> 1) - 1u));
 }
 
 // One candidate block scaling (block maximum mapped to M * s * s_g).
@@ -89,19 +124,28 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   r.scale = e4m3_rne(v);
   const float s = e4m3_value(r.scale);
   const float rs = s * sg;
-  const double s64 = (double)s, sg64 = (double)sg;
+  const double half_ss = 0.5 * ((double)s * (double)sg);   // exact: 4 + 24 significant bits
   r.codes = 0;
   r.err = 0.0;
+  if (rs > 0.0f) {
+    const E2m1Thresholds th = e2m1_thresholds(rs);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const uint32_t neg = __float_as_uint(u[i]) >> 31;
-    uint32_t idx = 0;
-    if (rs > 0.0f) idx = e2m1_index(fminf(fabsf(u[i]) / rs, 6.0f));
-    r.codes |= (uint64_t)((neg << 3) | idx) << (4 * i);
-    double dec = (e2m1_value64(idx) * s64) * sg64;   // exact: <= 30 significant bits
-    if (neg) dec = -dec;
-    const double d = (double)u[i] - dec;
-    r.err = r.err + d * d;
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t neg = __float_as_uint(u[i]) >> 31;
+      const uint32_t idx = e2m1_index_thr(fabsf(u[i]), th);
+      r.codes |= (uint64_t)((neg << 3) | idx) << (4 * i);
+      const double dec = (double)e2m1_twice(idx) * half_ss;   // exact q * s * s_g
+      const double d = (double)u[i] - (neg ? -dec : dec);
+      r.err = r.err + d * d;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t neg = __float_as_uint(u[i]) >> 31;
+      r.codes |= (uint64_t)(neg << 3) << (4 * i);
+      const double d = (double)u[i];
+      r.err = r.err + d * d;
+    }
   }
   return r;
 }

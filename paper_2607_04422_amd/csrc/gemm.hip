@@ -27,12 +27,24 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;        // output tile rows
-constexpr int BN = 128;        // output tile cols
-constexpr int KS = 64;         // K per LDS stage (4 NVFP4 blocks)
-constexpr int kThreads = 256;  // 4 waves in a 2 x 2 grid, 64 x 64 outputs each
+// Tile configuration of the exact NVFP4 product: WAVES_M x WAVES_N waves, each
+// owning TM x TN MFMA 32x32 tiles; K is staged through LDS 64 elements (four
+// NVFP4 blocks) at a time, double-buffered.
+#ifndef FP4R_FP4_WAVES_M
+#define FP4R_FP4_WAVES_M 4
+#endif
+#ifndef FP4R_FP4_WAVES_N
+#define FP4R_FP4_WAVES_N 2
+#endif
+#ifndef FP4R_FP4_TM
+#define FP4R_FP4_TM 1
+#endif
+#ifndef FP4R_FP4_TN
+#define FP4R_FP4_TN 2
+#endif
+constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
 
-// LDS element (row, k) of a 128 x 64 16-bit tile: 16-byte chunks XOR-swizzled by row.
+// LDS element (row, k) of a ROWS x 64 16-bit tile: 16-byte chunks XOR-swizzled by row.
 FP4R_DEV int lds_idx(int row, int chunk) { return row * KS + ((chunk ^ (row & 7)) << 3); }
 
 // Output tile coordinates.  Symmetric products enumerate the upper triangle
@@ -54,26 +66,29 @@ FP4R_DEV void tile_coords(int64_t t, int tiles_m, int tiles_n, bool sym, int& tm
 }
 
 // ---------------------------------------------------------------------------
-// NVFP4 operand staging.
+// NVFP4 operand staging: each thread loads whole 16-element blocks (8 code
+// bytes + 1 scale byte), decodes them to f16 and writes them to LDS.
 
+template <int ROWS, int NT>
 struct Fp4Stage {
-  uint2 codes[2];
-  uint32_t scales[2];
+  static constexpr int kPer = ROWS * 4 / NT;   // blocks per thread per stage
+  uint2 codes[kPer];
+  uint32_t scales[kPer];
 };
 
+template <int ROWS, int NT>
 FP4R_DEV void fp4_load(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t K, int64_t row0,
-                       int stage, Fp4Stage& s) {
-  const int r = threadIdx.x >> 1, h = threadIdx.x & 1;
-  const int64_t grow = row0 + r;
+                       int stage, Fp4Stage<ROWS, NT>& s) {
   const int64_t nkb = K / 16;
-  const uint8_t* codes = op.codes + mat * op.codes_bstride + grow * (K / 2);
-  const uint8_t* scales = op.scales + mat * op.scales_bstride + grow * nkb;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int64_t kb = (int64_t)stage * 4 + 2 * h + j;
+  for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
+    const int idx = threadIdx.x + NT * j;
+    const int r = idx >> 2;
+    const int64_t kb = (int64_t)stage * 4 + (idx & 3);
+    const int64_t grow = row0 + r;
     if (grow < rows && kb < nkb) {
-      s.codes[j] = *reinterpret_cast<const uint2*>(codes + kb * 8);
-      s.scales[j] = scales[kb];
+      s.codes[j] = *reinterpret_cast<const uint2*>(op.codes + mat * op.codes_bstride + grow * (K / 2) + kb * 8);
+      s.scales[j] = op.scales[mat * op.scales_bstride + grow * nkb + kb];
     } else {
       s.codes[j] = make_uint2(0u, 0u);
       s.scales[j] = 0u;
@@ -88,10 +103,12 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
   return q * s2;
 }
 
-FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage& s) {
-  const int r = threadIdx.x >> 1, h = threadIdx.x & 1;
+template <int ROWS, int NT>
+FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage<ROWS, NT>& s) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
+    const int idx = threadIdx.x + NT * j;
+    const int r = idx >> 2, kb = idx & 3;
     const _Float16 sv = (_Float16)e4m3_value(s.scales[j]);
     const f16x2 s2 = {sv, sv};
     const uint32_t w[2] = {s.codes[j].x, s.codes[j].y};
@@ -102,8 +119,7 @@ FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage& s) {
       const f16x2 p2 = fp4_pair<2>(w[half], s2), p3 = fp4_pair<3>(w[half], s2);
       v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
-      const int chunk = (2 * h + j) * 2 + half;
-      *reinterpret_cast<f16x8*>(lds + lds_idx(r, chunk)) = v;
+      *reinterpret_cast<f16x8*>(lds + lds_idx(r, kb * 2 + half)) = v;
     }
   }
 }
@@ -111,131 +127,224 @@ FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage& s) {
 // ---------------------------------------------------------------------------
 // Exact NVFP4 product.
 
-template <int MODE>
-__global__ __launch_bounds__(kThreads) void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n,
-                                                       int64_t tiles_per_mat) {
-  __shared__ _Float16 lds[2][2][BM * KS];
+#ifndef FP4R_FP4_WAVES_PER_EU
+#define FP4R_FP4_WAVES_PER_EU 4
+#endif
+
+template <int MODE, int WM_, int WN_, int TM, int TN>
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
+void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) {
+  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
+  constexpr int kLdT = BN + 1;   // padded row of the FP32 output tile staged in LDS
+  constexpr size_t kMainBytes = (size_t)2 * (BM + BN) * KS * sizeof(_Float16);
+  constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
+  __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
+  _Float16(*lds_a)[BM * KS] = reinterpret_cast<_Float16(*)[BM * KS]>(smem);
+  _Float16(*lds_b)[BN * KS] = reinterpret_cast<_Float16(*)[BN * KS]>(smem + 2 * BM * KS * sizeof(_Float16));
   constexpr bool kSym = MODE != kModeUpdateX;
   const int64_t mat = blockIdx.x / tiles_per_mat;
   int tm, tn;
   tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN_, wn = wave % WN_;
   const int64_t nkb = g.K / 16;
   const int nstages = (int)((nkb + 3) / 4);
 
-  double acc[2][2][16];
+  double acc[TM][TN][16];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0;
 
-  Fp4Stage sa, sb;
-  fp4_load(g.a, mat, g.M, g.K, row0, 0, sa);
-  fp4_load(g.b, mat, g.N, g.K, col0, 0, sb);
-  fp4_store(lds[0][0], sa);
-  fp4_store(lds[0][1], sb);
+  Fp4Stage<BM, NT> sa;
+  Fp4Stage<BN, NT> sb;
+  fp4_load<BM, NT>(g.a, mat, g.M, g.K, row0, 0, sa);
+  fp4_load<BN, NT>(g.b, mat, g.N, g.K, col0, 0, sb);
+  fp4_store<BM, NT>(lds_a[0], sa);
+  fp4_store<BN, NT>(lds_b[0], sb);
   __syncthreads();
 
   const f32x16 zero = {};
   for (int s = 0; s < nstages; ++s) {
     const int buf = s & 1;
     if (s + 1 < nstages) {
-      fp4_load(g.a, mat, g.M, g.K, row0, s + 1, sa);
-      fp4_load(g.b, mat, g.N, g.K, col0, s + 1, sb);
+      fp4_load<BM, NT>(g.a, mat, g.M, g.K, row0, s + 1, sa);
+      fp4_load<BN, NT>(g.b, mat, g.N, g.K, col0, s + 1, sb);
     }
-    const _Float16* la = lds[buf][0];
-    const _Float16* lb = lds[buf][1];
+    const _Float16* la = lds_a[buf];
+    const _Float16* lb = lds_b[buf];
     const int kbs = (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4);
     for (int kb = 0; kb < kbs; ++kb) {
       const int chunk = kb * 2 + (lane >> 5);
-      f16x8 af[2], bfr[2];
+      f16x8 af[TM], bfr[TN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx(wm * 64 + i * 32 + (lane & 31), chunk));
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx(wn * 64 + j * 32 + (lane & 31), chunk));
-      f32x16 p[2][2];
+      for (int j = 0; j < TN; ++j)
+        bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
+        for (int j = 0; j < TN; ++j) {
+          const f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
+          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[e];
+        }
     }
     if (s + 1 < nstages) {
-      fp4_store(lds[buf ^ 1][0], sa);
-      fp4_store(lds[buf ^ 1][1], sb);
+      fp4_store<BM, NT>(lds_a[buf ^ 1], sa);
+      fp4_store<BN, NT>(lds_b[buf ^ 1], sb);
     }
     __syncthreads();
   }
 
-  // epilogue: binary64 formula, one rounding to binary32
+  // epilogue: binary64 formula, one rounding to binary32, staged through LDS
+  // (the main loop's buffers are free after the last barrier)
   const double sga = (double)g.sc[mat].sg[g.slot_a], sgb = (double)g.sc[mat].sg[g.slot_b];
   const double alpha = sga * sgb;   // exact: product of two binary32 values
   const double ca = (double)g.ca, cb = (double)g.cb, cc = (double)g.cc;
   float* out = g.out + mat * g.out_bstride;
   const float* aux = g.aux ? g.aux + mat * g.out_bstride : nullptr;
-  const bool mirror = kSym && tm != tn;
+  float* tile = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t r = row0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int64_t c = col0 + wn * 64 + j * 32 + (lane & 31);
+        const int rl = (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int cl = (wn * TN + j) * 32 + (lane & 31);
+        const int64_t r = row0 + rl, c = col0 + cl;
+        float f = 0.0f;
         if (r < g.M && c < g.N) {
           double v = alpha * acc[i][j][e];
           if (MODE == kModeGramB) v = cb * (double)aux[r * g.N + c] + cc * v;
           if (MODE == kModeUpdateX) v = ca * (double)aux[r * g.N + c] + v;
-          const float f = (float)v;
-          out[r * g.N + c] = f;
-          if (mirror) out[c * g.N + r] = f;
+          f = (float)v;
         }
+        tile[rl * kLdT + cl] = f;
       }
+  __syncthreads();
+  // coalesced stores: rows of the tile, and (off-diagonal symmetric tiles) its transpose
+  const bool mirror = kSym && tm != tn;
+  constexpr int kSegs = BN / 16;                 // 16-float segments per row
+  for (int idx = threadIdx.x; idx < BM * kSegs; idx += NT) {
+    const int rl = idx / kSegs, q = idx % kSegs;
+    const int64_t r = row0 + rl, c = col0 + 16 * q;
+    if (r < g.M && c < g.N) {
+      float4* dst = reinterpret_cast<float4*>(out + r * g.N + c);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        dst[k] = make_float4(tile[rl * kLdT + 16 * q + 4 * k], tile[rl * kLdT + 16 * q + 4 * k + 1],
+                             tile[rl * kLdT + 16 * q + 4 * k + 2], tile[rl * kLdT + 16 * q + 4 * k + 3]);
+    }
+    if (mirror) {
+      // row cl of the mirrored tile = column cl of this tile
+      const int cl = rl;
+      const int64_t mr = col0 + cl, mc = row0 + 16 * q;
+      if (mr < g.N && mc < g.M) {
+        float4* dst = reinterpret_cast<float4*>(out + mr * g.N + mc);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          dst[k] = make_float4(tile[(16 * q + 4 * k) * kLdT + cl], tile[(16 * q + 4 * k + 1) * kLdT + cl],
+                               tile[(16 * q + 4 * k + 2) * kLdT + cl], tile[(16 * q + 4 * k + 3) * kLdT + cl]);
+      }
+    }
+  }
+  // rotated amaxes of the output: 16-column blocks of every row, and 16-row blocks
+  // of every column (the mirrored tile's rows, or X_{k+1} along m)
+  const bool do_rows = g.amax_row_slot >= 0;
+  const bool do_cols = g.amax_col_slot >= 0 && (!kSym || mirror);
+  float rmax = 0.0f, cmax = 0.0f;
+  if (do_rows) {
+    for (int idx = threadIdx.x; idx < BM * kSegs; idx += NT) {
+      const int rl = idx / kSegs, q = idx % kSegs;
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[rl * kLdT + 16 * q + k];
+      if (g.amax_rotate) rotate16(u, g.amax_mask);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) rmax = fmaxf(rmax, fabsf(u[k]));
+    }
+  }
+  if (do_cols) {
+    constexpr int kRsegs = BM / 16;
+    for (int idx = threadIdx.x; idx < BN * kRsegs; idx += NT) {
+      const int cl = idx % BN, q = idx / BN;
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[(16 * q + k) * kLdT + cl];
+      if (g.amax_rotate) rotate16(u, g.amax_mask);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) cmax = fmaxf(cmax, fabsf(u[k]));
+    }
+  }
+  if (do_rows) {
+    const float w = warp_max(rmax);
+    if (lane == 0) atomicMax(&g.sc[mat].amax[g.amax_row_slot], __float_as_uint(w));
+  }
+  if (do_cols) {
+    const float w = warp_max(cmax);
+    if (lane == 0) atomicMax(&g.sc[mat].amax[g.amax_col_slot], __float_as_uint(w));
+  }
 }
 
 hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st) {
+  constexpr int WM_ = FP4R_FP4_WAVES_M, WN_ = FP4R_FP4_WAVES_N, TM = FP4R_FP4_TM, TN = FP4R_FP4_TN;
+  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
+  static_assert(BM == BN, "symmetric products need square tiles");
+  static_assert((BM * 4) % NT == 0, "each thread stages whole blocks");
   const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
   const bool sym = mode != kModeUpdateX;
   const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
   const dim3 grid((uint32_t)(per * g.batch));
   switch (mode) {
     case kModeGramA:
-      hipLaunchKernelGGL(k_gemm_fp4<kModeGramA>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_fp4<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
       break;
     case kModeGramB:
-      hipLaunchKernelGGL(k_gemm_fp4<kModeGramB>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_fp4<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
       break;
     default:
-      hipLaunchKernelGGL(k_gemm_fp4<kModeUpdateX>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_fp4<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
   }
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// BF16 comparison product.
+// BF16 comparison product: plain MFMA accumulation in binary32.
 
+#ifndef FP4R_BF16_WAVES_M
+#define FP4R_BF16_WAVES_M 4
+#endif
+#ifndef FP4R_BF16_WAVES_N
+#define FP4R_BF16_WAVES_N 2
+#endif
+#ifndef FP4R_BF16_TM
+#define FP4R_BF16_TM 2
+#endif
+#ifndef FP4R_BF16_TN
+#define FP4R_BF16_TN 4
+#endif
+
+template <int ROWS, int NT>
 struct Bf16Stage {
-  uint4 v[4];
+  static constexpr int kPer = ROWS * 8 / NT;   // 16-byte chunks per thread per stage
+  uint4 v[kPer];
 };
 
+template <int ROWS, int NT>
 FP4R_DEV void bf16_load(const uint16_t* base, int64_t rows, int64_t K, int64_t row0, int stage,
-                        Bf16Stage& s) {
-  const int chunk = threadIdx.x & 7;
-  const int64_t k = (int64_t)stage * KS + chunk * 8;
+                        Bf16Stage<ROWS, NT>& s) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t grow = row0 + (threadIdx.x >> 3) + 32 * q;
+  for (int q = 0; q < Bf16Stage<ROWS, NT>::kPer; ++q) {
+    const int idx = threadIdx.x + NT * q;
+    const int64_t grow = row0 + (idx >> 3);
+    const int64_t k = (int64_t)stage * KS + (idx & 7) * 8;
     if (grow < rows && k < K)
       s.v[q] = *reinterpret_cast<const uint4*>(base + grow * K + k);
     else
@@ -243,12 +352,12 @@ FP4R_DEV void bf16_load(const uint16_t* base, int64_t rows, int64_t K, int64_t r
   }
 }
 
-FP4R_DEV void bf16_store(uint16_t* lds, const Bf16Stage& s) {
-  const int chunk = threadIdx.x & 7;
+template <int ROWS, int NT>
+FP4R_DEV void bf16_store(uint16_t* lds, const Bf16Stage<ROWS, NT>& s) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = (threadIdx.x >> 3) + 32 * q;
-    *reinterpret_cast<uint4*>(lds + lds_idx(r, chunk)) = s.v[q];
+  for (int q = 0; q < Bf16Stage<ROWS, NT>::kPer; ++q) {
+    const int idx = threadIdx.x + NT * q;
+    *reinterpret_cast<uint4*>(lds + lds_idx(idx >> 3, idx & 7)) = s.v[q];
   }
 }
 
@@ -259,60 +368,63 @@ FP4R_DEV uint16_t to_bf16(float f) {
 
 FP4R_DEV float from_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-template <int MODE>
-__global__ __launch_bounds__(kThreads) void k_gemm_bf16(GemmBf16Args g, int tiles_m, int tiles_n,
-                                                        int64_t tiles_per_mat) {
-  __shared__ uint16_t lds[2][2][BM * KS];
+template <int MODE, int WM_, int WN_, int TM, int TN>
+__global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int tiles_m, int tiles_n,
+                                                             int64_t tiles_per_mat) {
+  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
+  __shared__ uint16_t lds_a[2][BM * KS];
+  __shared__ uint16_t lds_b[2][BN * KS];
   constexpr bool kSym = MODE != kModeUpdateX;
   const int64_t mat = blockIdx.x / tiles_per_mat;
   int tm, tn;
   tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN_, wn = wave % WN_;
   const int nstages = (int)((g.K + KS - 1) / KS);
   const uint16_t* A = g.a + mat * g.a_bstride;
   const uint16_t* B = g.b + mat * g.b_bstride;
 
-  f32x16 acc[2][2];
+  f32x16 acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
-  Bf16Stage sa, sb;
-  bf16_load(A, g.M, g.K, row0, 0, sa);
-  bf16_load(B, g.N, g.K, col0, 0, sb);
-  bf16_store(lds[0][0], sa);
-  bf16_store(lds[0][1], sb);
+  Bf16Stage<BM, NT> sa;
+  Bf16Stage<BN, NT> sb;
+  bf16_load<BM, NT>(A, g.M, g.K, row0, 0, sa);
+  bf16_load<BN, NT>(B, g.N, g.K, col0, 0, sb);
+  bf16_store<BM, NT>(lds_a[0], sa);
+  bf16_store<BN, NT>(lds_b[0], sb);
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
     const int buf = s & 1;
     if (s + 1 < nstages) {
-      bf16_load(A, g.M, g.K, row0, s + 1, sa);
-      bf16_load(B, g.N, g.K, col0, s + 1, sb);
+      bf16_load<BM, NT>(A, g.M, g.K, row0, s + 1, sa);
+      bf16_load<BN, NT>(B, g.N, g.K, col0, s + 1, sb);
     }
-    const uint16_t* la = lds[buf][0];
-    const uint16_t* lb = lds[buf][1];
+    const uint16_t* la = lds_a[buf];
+    const uint16_t* lb = lds_b[buf];
     const int64_t krem = g.K - (int64_t)s * KS;
     const int kbs = (int)(krem < KS ? krem / 16 : 4);
     for (int kb = 0; kb < kbs; ++kb) {
       const int chunk = kb * 2 + (lane >> 5);
-      bf16x8 af[2], bfr[2];
+      bf16x8 af[TM], bfr[TN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(la + lds_idx(wm * 64 + i * 32 + (lane & 31), chunk));
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(lb + lds_idx(wn * 64 + j * 32 + (lane & 31), chunk));
+      for (int j = 0; j < TN; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
     if (s + 1 < nstages) {
-      bf16_store(lds[buf ^ 1][0], sa);
-      bf16_store(lds[buf ^ 1][1], sb);
+      bf16_store<BM, NT>(lds_a[buf ^ 1], sa);
+      bf16_store<BN, NT>(lds_b[buf ^ 1], sb);
     }
     __syncthreads();
   }
@@ -323,13 +435,13 @@ __global__ __launch_bounds__(kThreads) void k_gemm_bf16(GemmBf16Args g, int tile
   float* X = g.x ? g.x + mat * g.x_bstride : nullptr;
   uint16_t* o16t = g.out16t ? g.out16t + mat * g.out16t_bstride : nullptr;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t r = row0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int64_t c = col0 + wn * 64 + j * 32 + (lane & 31);
+        const int64_t r = row0 + (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int64_t c = col0 + (wn * TN + j) * 32 + (lane & 31);
         if (r < g.M && c < g.N) {
           float v = acc[i][j][e];
           if (MODE == kModeGramB) v = g.cb * from_bf16(aux16[r * g.N + c]) + g.cc * v;
@@ -349,19 +461,23 @@ __global__ __launch_bounds__(kThreads) void k_gemm_bf16(GemmBf16Args g, int tile
 }
 
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st) {
+  constexpr int WM_ = FP4R_BF16_WAVES_M, WN_ = FP4R_BF16_WAVES_N, TM = FP4R_BF16_TM, TN = FP4R_BF16_TN;
+  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
+  static_assert(BM == BN, "symmetric products need square tiles");
+  static_assert((BM * 8) % NT == 0, "each thread stages whole 16-byte chunks");
   const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
   const bool sym = mode != kModeUpdateX;
   const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
   const dim3 grid((uint32_t)(per * g.batch));
   switch (mode) {
     case kModeGramA:
-      hipLaunchKernelGGL(k_gemm_bf16<kModeGramA>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_bf16<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
       break;
     case kModeGramB:
-      hipLaunchKernelGGL(k_gemm_bf16<kModeGramB>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_bf16<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
       break;
     default:
-      hipLaunchKernelGGL(k_gemm_bf16<kModeUpdateX>, grid, dim3(kThreads), 0, st, g, tiles_m, tiles_n, per);
+      hipLaunchKernelGGL((k_gemm_bf16<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
   }
   return hipGetLastError();
 }

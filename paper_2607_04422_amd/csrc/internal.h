@@ -31,16 +31,19 @@ struct MatChunk {
 
 // Per-matrix scalars kept in the workspace (one struct per matrix).
 struct MatScalars {
-  uint32_t amax[4];      // bit patterns: X along n, X along m, A, B
-  float sg[4];           // tensor scales derived from amax
+  uint32_t amax[6];      // bit patterns: X along n / along m (two pairs, alternating by step), A, B
+  float sg[6];           // tensor scales derived from amax
   float tau;             // clip threshold (+inf without clipping)
   float inv_norm;        // 1 / (||X'||_F + eps)
   uint32_t sel_prefix[2];  // radix select state for ranks lo and lo + 1
   uint32_t sel_rank[2];
-  uint32_t pad[2];
 };
 
-constexpr int kSlotXn = 0, kSlotXm = 1, kSlotA = 2, kSlotB = 3;
+// amax / tensor-scale slots.  The X slots alternate between steps so that the
+// update product of step k can record the amaxes of X_{k+1} while step k still
+// reads those of X_k.
+constexpr int kSlotXn = 0, kSlotXm = 1, kSlotA = 4, kSlotB = 5;
+constexpr int kNumSlots = 6;
 
 // Radix select histogram: [2 ranks][2048 bins] per matrix.
 constexpr int kHistBins = 2048;
@@ -63,9 +66,10 @@ hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, 
 
 // Canonical copy: X_b (m x n, m = min(rows, cols)) = fl32(clamp(M, tau) * inv_norm),
 // transposed when rows > cols.  x: base of the group's canonical buffer, matrix b
-// of the chunk at x + (first + b) * x_bstride.
-hipError_t launch_prep_copy(const MatChunk& ch, const MatScalars* sc, float* x,
-                            int64_t x_bstride, hipStream_t st);
+// of the chunk at x + (first + b) * x_bstride.  Also records the amaxes of X_b
+// rotated along n and along m (Hadamard signs `mask`) in slots slot_n, slot_m.
+hipError_t launch_prep_copy(const MatChunk& ch, MatScalars* sc, float* x, int64_t x_bstride,
+                            uint32_t mask, bool rotate, int slot_n, int slot_m, hipStream_t st);
 
 // Copy-out: caller out (rows x cols) from canonical X (transposed when rows > cols).
 hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride,
@@ -95,6 +99,12 @@ hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rot
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st);
 
+// Both quantisations of X (m x n, row stride n) from one read: qX along n into
+// qx (slot_n), qXt along m into qxt (slot_m, stored transposed).
+hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
+                            uint32_t sign_mask, bool rotate, bool adaptive46, MatScalars* sc,
+                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st);
+
 // ---------------------------------------------------------------------------
 // GEMMs (all operands K-contiguous: C[i][j] = sum_k A[i][k] B[j][k]).
 
@@ -109,8 +119,14 @@ struct Fp4Operand {
 struct GemmFp4Args {
   Fp4Operand a, b;
   int64_t M, N, K, batch;
-  const MatScalars* sc;   // tensor scales per matrix
+  MatScalars* sc;         // tensor scales per matrix (and amax records written by the epilogue)
   int slot_a, slot_b;
+  // Epilogue amax of the output rotated with `amax_mask`: 16-column blocks into
+  // slot amax_row_slot, 16-row blocks into amax_col_slot (symmetric products:
+  // the mirrored lower tiles' row blocks); -1 disables.
+  int amax_row_slot, amax_col_slot;
+  uint32_t amax_mask;
+  int amax_rotate;        // 0: amax of the plain values (no Hadamard)
   float* out;             // FP32 [M][N] per matrix (ld = N)
   int64_t out_bstride;
   const float* aux;       // kModeGramB: A (may equal out); kModeUpdateX: X_k (may equal out)
@@ -143,9 +159,9 @@ hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st
 hipError_t launch_cast_bf16(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
                             uint16_t* xb, uint16_t* xbt, int64_t b_bstride, hipStream_t st);
 
-// Zero the amax slots of n scalar records; `full` also resets tensor scales,
-// tau (+inf) and inv_norm (1).
-hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, bool full, hipStream_t st);
+// Zero the amax slots selected by `slot_mask` (bit i = slot i) of n scalar
+// records; `full` also resets every tensor scale, tau (+inf) and inv_norm (1).
+hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, uint32_t slot_mask, bool full, hipStream_t st);
 
 // out[i] = sc[i].tau (which = 0) or sc[i].sg[slot] (which = 1).
 hipError_t launch_export_scalar(const MatScalars* sc, int64_t n, int which, int slot, float* out,

@@ -223,13 +223,87 @@ hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, 
 
 constexpr int kT = 64;
 
-FP4R_DEV int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// dir 0 (prep): canonical X = fl32(clamp(M) * inv), transposed when rows > cols.
-// dir 1 (copy-out): M_out = X (transposed back when rows > cols).
-template <int DIR>
-__global__ __launch_bounds__(256) void k_tile_copy(MatChunk ch, const MatScalars* sc, float* xbase,
-                                                   int64_t x_bstride) {
+// Block-wide max of non-negative floats; thread 0 returns the result.
+FP4R_DEV float block_max_256(float v, float* red) {
+  v = warp_max(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// Prep: canonical X = fl32(clamp(M) * inv) (transposed when rows > cols), staged
+// through a 64 x 64 LDS tile that also yields the amaxes of X rotated along n
+// (16-column blocks) and along m (16-row blocks) for the first NS step.
+__global__ __launch_bounds__(256) void k_prep_copy(MatChunk ch, MatScalars* sc, float* xbase,
+                                                   int64_t x_bstride, uint32_t mask, int rotate,
+                                                   int slot_n, int slot_m) {
+  __shared__ float tile[kT][kT + 1];
+  __shared__ float red[4];
+  const int64_t t = blockIdx.x;
+  const int mi = find_matrix(ch, t);
+  const MatDesc& d = ch.m[mi];
+  const bool tall = d.rows > d.cols;
+  const int64_t xm = tall ? d.cols : d.rows, xn = tall ? d.rows : d.cols;   // canonical m x n
+  const int64_t tcols = cdiv(xn, kT);
+  const int64_t tt = t - d.tile_begin;
+  const int64_t xr0 = (tt / tcols) * kT, xc0 = (tt % tcols) * kT;   // canonical tile origin
+  float* X = xbase + (int64_t)mi * x_bstride;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;   // 64 x 4
+  const float tau = sc[mi].tau;
+  const float inv = sc[mi].inv_norm;
+  // tile[i][j] = canonical X[xr0 + i][xc0 + j]
+  for (int i = ty; i < kT; i += 4) {
+    if (!tall) {
+      const int64_t r = xr0 + i, c = xc0 + tx;
+      if (r < xm && c < xn) tile[i][tx] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
+    } else {
+      // M row (xc0 + i), M column (xr0 + tx)  ->  X[xr0 + tx][xc0 + i]
+      const int64_t r = xc0 + i, c = xr0 + tx;
+      if (r < d.rows && c < d.cols) tile[tx][i] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
+    }
+  }
+  __syncthreads();
+  for (int i = ty; i < kT; i += 4) {
+    const int64_t r = xr0 + i, c = xc0 + tx;
+    if (r < xm && c < xn) X[r * xn + c] = tile[i][tx];
+  }
+  // rotated amaxes: thread -> one 16-column block and one 16-row block of the tile
+  float mr = 0.0f, mc = 0.0f;
+  {
+    const int i = threadIdx.x >> 2, b = threadIdx.x & 3;
+    if (xr0 + i < xm && xc0 + 16 * b < xn) {
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[i][16 * b + k];
+      if (rotate) rotate16(u, mask);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) mr = fmaxf(mr, fabsf(u[k]));
+    }
+  }
+  {
+    const int j = threadIdx.x & 63, b = threadIdx.x >> 6;
+    if (xc0 + j < xn && xr0 + 16 * b < xm) {
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[16 * b + k][j];
+      if (rotate) rotate16(u, mask);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) mc = fmaxf(mc, fabsf(u[k]));
+    }
+  }
+  const float br = block_max_256(mr, red);
+  __syncthreads();
+  const float bc = block_max_256(mc, red);
+  if (threadIdx.x == 0) {
+    atomicMax(&sc[mi].amax[slot_n], __float_as_uint(br));
+    atomicMax(&sc[mi].amax[slot_m], __float_as_uint(bc));
+  }
+}
+
+// Copy-out: caller M (rows x cols) from canonical X (transposed back when tall).
+__global__ __launch_bounds__(256) void k_copy_out(MatChunk ch, const float* xbase, int64_t x_bstride) {
   __shared__ float tile[kT][kT + 1];
   const int64_t t = blockIdx.x;
   const int mi = find_matrix(ch, t);
@@ -237,60 +311,37 @@ __global__ __launch_bounds__(256) void k_tile_copy(MatChunk ch, const MatScalars
   const bool tall = d.rows > d.cols;
   const int64_t tcols = cdiv(d.cols, kT);
   const int64_t tt = t - d.tile_begin;
-  const int64_t br = (tt / tcols) * kT, bc = (tt % tcols) * kT;  // tile origin in M coordinates
-  float* X = xbase + (int64_t)mi * x_bstride;
-  const int64_t xld = tall ? d.rows : d.cols;   // canonical row length n
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;   // 64 x 4
-  const float tau = DIR == 0 ? sc[mi].tau : 0.0f;
-  const float inv = DIR == 0 ? sc[mi].inv_norm : 0.0f;
+  const int64_t br = (tt / tcols) * kT, bc = (tt % tcols) * kT;   // tile origin in M coordinates
+  const float* X = xbase + (int64_t)mi * x_bstride;
+  const int64_t xld = tall ? d.rows : d.cols;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   if (!tall) {
     for (int i = ty; i < kT; i += 4) {
       const int64_t r = br + i, c = bc + tx;
-      if (r < d.rows && c < d.cols) {
-        if (DIR == 0) {
-          const float v = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau);
-          X[r * xld + c] = v * inv;
-        } else {
-          d.out[r * d.ld_out + c] = X[r * xld + c];
-        }
-      }
+      if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = X[r * xld + c];
     }
     return;
   }
-  // tall: X[c][r] <-> M[r][c]
-  if (DIR == 0) {
-    for (int i = ty; i < kT; i += 4) {
-      const int64_t r = br + i, c = bc + tx;
-      if (r < d.rows && c < d.cols) tile[i][tx] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
-    }
-    __syncthreads();
-    for (int i = ty; i < kT; i += 4) {
-      const int64_t c = bc + i, r = br + tx;   // X row c, column r
-      if (r < d.rows && c < d.cols) X[c * xld + r] = tile[tx][i];
-    }
-  } else {
-    for (int i = ty; i < kT; i += 4) {
-      const int64_t c = bc + i, r = br + tx;
-      if (r < d.rows && c < d.cols) tile[tx][i] = X[c * xld + r];
-    }
-    __syncthreads();
-    for (int i = ty; i < kT; i += 4) {
-      const int64_t r = br + i, c = bc + tx;
-      if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = tile[i][tx];
-    }
+  for (int i = ty; i < kT; i += 4) {
+    const int64_t c = bc + i, r = br + tx;
+    if (r < d.rows && c < d.cols) tile[tx][i] = X[c * xld + r];
+  }
+  __syncthreads();
+  for (int i = ty; i < kT; i += 4) {
+    const int64_t r = br + i, c = bc + tx;
+    if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = tile[i][tx];
   }
 }
 
-hipError_t launch_prep_copy(const MatChunk& ch, const MatScalars* sc, float* x, int64_t x_bstride,
-                            hipStream_t st) {
-  hipLaunchKernelGGL(k_tile_copy<0>, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, x,
-                     x_bstride);
+hipError_t launch_prep_copy(const MatChunk& ch, MatScalars* sc, float* x, int64_t x_bstride,
+                            uint32_t mask, bool rotate, int slot_n, int slot_m, hipStream_t st) {
+  hipLaunchKernelGGL(k_prep_copy, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, x,
+                     x_bstride, mask, (int)rotate, slot_n, slot_m);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride, hipStream_t st) {
-  hipLaunchKernelGGL(k_tile_copy<1>, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch,
-                     (const MatScalars*)nullptr, const_cast<float*>(x), x_bstride);
+  hipLaunchKernelGGL(k_copy_out, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, x, x_bstride);
   return hipGetLastError();
 }
 
@@ -395,6 +446,79 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   out.scales[b * out.scales_bstride + scale_off] = (uint8_t)scale;
 }
 
+// Both quantisations of X from one read: a 64 x 64 tile is staged in LDS; each
+// thread encodes one 16-column block (qX, along n) and one 16-row block (qXt,
+// along m, written transposed).
+__global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
+                                                   uint32_t mask, int rotate, int adaptive, MatScalars* sc,
+                                                   int slot_n, int slot_m, QOut qx, QOut qxt) {
+  __shared__ float tile[kT][kT + 1];
+  const int64_t b = blockIdx.y;
+  const int64_t tn = cdiv(n, kT);
+  const int64_t r0 = (blockIdx.x / tn) * kT, c0 = (blockIdx.x % tn) * kT;
+  const float* X = x + b * x_bstride;
+  const float sgn = tensor_scale_from_amax(sc[b].amax[slot_n]);
+  const float sgm = tensor_scale_from_amax(sc[b].amax[slot_m]);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    sc[b].sg[slot_n] = sgn;
+    sc[b].sg[slot_m] = sgm;
+  }
+  {
+    const int i = threadIdx.x >> 2, q = threadIdx.x & 3;   // row i, 16 columns at 16 q
+    if (r0 + i < m && c0 + 16 * q < n) {
+      const float4* p = reinterpret_cast<const float4*>(X + (r0 + i) * n + c0 + 16 * q);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float4 v = p[k];
+        tile[i][16 * q + 4 * k] = v.x; tile[i][16 * q + 4 * k + 1] = v.y;
+        tile[i][16 * q + 4 * k + 2] = v.z; tile[i][16 * q + 4 * k + 3] = v.w;
+      }
+    }
+  }
+  __syncthreads();
+  {
+    const int i = threadIdx.x >> 2, q = threadIdx.x & 3;
+    const int64_t r = r0 + i, c = c0 + 16 * q;
+    if (r < m && c < n) {
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[i][16 * q + k];
+      if (rotate) rotate16(u, mask);
+      uint32_t scale;
+      uint64_t codes;
+      quant_block(u, sgn, adaptive != 0, scale, codes);
+      *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + r * (n / 2) + c / 2) =
+          make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+      qx.scales[b * qx.scales_bstride + r * (n / 16) + c / 16] = (uint8_t)scale;
+    }
+  }
+  {
+    const int j = threadIdx.x & 63, q = threadIdx.x >> 6;   // column j, 16 rows at 16 q
+    const int64_t c = c0 + j, r = r0 + 16 * q;
+    if (r < m && c < n) {
+      float u[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) u[k] = tile[16 * q + k][j];
+      if (rotate) rotate16(u, mask);
+      uint32_t scale;
+      uint64_t codes;
+      quant_block(u, sgm, adaptive != 0, scale, codes);
+      *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + c * (m / 2) + r / 2) =
+          make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+      qxt.scales[b * qxt.scales_bstride + c * (m / 16) + r / 16] = (uint8_t)scale;
+    }
+  }
+}
+
+hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
+                            uint32_t sign_mask, bool rotate, bool adaptive46, MatScalars* sc,
+                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st) {
+  const dim3 grid((uint32_t)(cdiv(m, kT) * cdiv(n, kT)), (uint32_t)batch);
+  hipLaunchKernelGGL(k_encode_x2, grid, dim3(256), 0, st, x, m, n, x_bstride, sign_mask, (int)rotate,
+                     (int)adaptive46, sc, slot_n, slot_m, qx, qxt);
+  return hipGetLastError();
+}
+
 hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                        MatScalars* sc, int slot, uint32_t* status, hipStream_t st) {
   const int64_t nblk = in.rows * in.cols / 16;
@@ -466,24 +590,25 @@ hipError_t launch_cast_bf16(const float* x, int64_t batch, int64_t m, int64_t n,
 // ---------------------------------------------------------------------------
 // Small per-matrix scalar kernels.
 
-__global__ void k_reset_scalars(MatScalars* sc, int64_t n, int full) {
+__global__ void k_reset_scalars(MatScalars* sc, int64_t n, uint32_t slot_mask, int full) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   MatScalars& s = sc[i];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) s.amax[k] = 0u;
+  for (int k = 0; k < kNumSlots; ++k)
+    if ((slot_mask >> k) & 1u) s.amax[k] = 0u;
   if (full) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) s.sg[k] = 0.0f;
+    for (int k = 0; k < kNumSlots; ++k) s.sg[k] = 0.0f;
     s.tau = __uint_as_float(0x7F800000u);   // +inf: clamping is the identity
     s.inv_norm = 1.0f;
   }
 }
 
-hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, bool full, hipStream_t st) {
+hipError_t launch_reset_scalars(MatScalars* sc, int64_t n, uint32_t slot_mask, bool full, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_reset_scalars, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, st, sc, n,
-                     (int)full);
+                     slot_mask, (int)full);
   return hipGetLastError();
 }
 
