@@ -130,6 +130,9 @@ FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage<ROWS, NT>& s) {
 #ifndef FP4R_FP4_WAVES_PER_EU
 #define FP4R_FP4_WAVES_PER_EU 4
 #endif
+#ifndef FP4R_FP4_PIPELINE
+#define FP4R_FP4_PIPELINE 0
+#endif
 
 template <int MODE, int WM_, int WN_, int TM, int TN>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
@@ -177,6 +180,53 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     const _Float16* la = lds_a[buf];
     const _Float16* lb = lds_b[buf];
     const int kbs = (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4);
+#if FP4R_FP4_PIPELINE
+    // Software pipeline over the stage's (block, tile) jobs: the MFMA of job t+1
+    // is in flight while the block sums of job t are folded into binary64.
+    {
+      constexpr int kJobs = TM * TN;
+      f16x8 af[TM], bfr[TN];
+      f32x16 pend;
+      int pend_i = 0, pend_j = 0;
+      bool have = false;
+      for (int kb = 0; kb < kbs; ++kb) {
+        const int chunk = kb * 2 + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
+#pragma unroll
+        for (int t = 0; t < kJobs; ++t) {
+          const int i = t / TN, j = t % TN;
+          const f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
+          if (have) {
+#pragma unroll
+            for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+              for (int jj = 0; jj < TN; ++jj)
+                if (ii == pend_i && jj == pend_j)
+#pragma unroll
+                  for (int e = 0; e < 16; ++e) acc[ii][jj][e] = acc[ii][jj][e] + (double)pend[e];
+          }
+          pend = p;
+          pend_i = i;
+          pend_j = j;
+          have = true;
+        }
+      }
+      if (have) {
+#pragma unroll
+        for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+          for (int jj = 0; jj < TN; ++jj)
+            if (ii == pend_i && jj == pend_j)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) acc[ii][jj][e] = acc[ii][jj][e] + (double)pend[e];
+      }
+    }
+#else
     for (int kb = 0; kb < kbs; ++kb) {
       const int chunk = kb * 2 + (lane >> 5);
       f16x8 af[TM], bfr[TN];
@@ -195,6 +245,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
           for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[e];
         }
     }
+#endif
     if (s + 1 < nstages) {
       fp4_store<BM, NT>(lds_a[buf ^ 1], sa);
       fp4_store<BN, NT>(lds_b[buf ^ 1], sb);
