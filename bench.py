@@ -56,6 +56,32 @@ def time_calls(fn, warmup, iters, torch):
     return (time.perf_counter() - t0) / iters
 
 
+def torch_bf16_reference(inputs, coeffs_for, steps, warmup, iters, torch):
+    """The same five BF16 NS steps written with torch.bmm (hipBLASLt), as context for the
+    in-library BF16 path: X bf16, A = X X^T, B = b A + c A A, X = a X + B X, batched per shape
+    group, on inputs already clipped, normalised and oriented short side first."""
+    groups = {}
+    for t in inputs:
+        r, c = t.shape
+        x = t if r <= c else t.t()
+        groups.setdefault((min(r, c), max(r, c)), []).append(x)
+    xs = {k: torch.stack([(v / v.norm()).to(torch.bfloat16) for v in vs]).contiguous() for k, vs in groups.items()}
+
+    def run():
+        for (m, n), x0 in xs.items():
+            co = coeffs_for(m, n)
+            x = x0
+            for (a, b, c) in co[:steps]:
+                xt = x.transpose(1, 2).contiguous()
+                A = torch.bmm(x, xt)
+                B = b * A + c * torch.bmm(A, A)
+                x = a * x + torch.bmm(B, x)
+        return x
+
+    t = time_calls(run, warmup, iters, torch)
+    return t
+
+
 def cpu_baseline(case, coeffs_for, steps):
     """The oracle, as it stands, on one matrix of the workload; FLOP-scaled to the whole set."""
     import numpy as np
@@ -168,6 +194,14 @@ def main():
                 "pct_bf16_peak": round(100 * flop / t16 / 1e12 / BF16_MFMA_PEAK_TFLOPS, 2),
                 "nvfp4_speedup_vs_bf16": round(t16 / t_step, 3)}
         del orth16
+        try:
+            tt = torch_bf16_reference(inputs, lambda r, c: F.fp4root_default_coeffs(r, c, S), S,
+                                      args.warmup, args.steps, torch)
+            bf16["torch_bmm_reference"] = {
+                "ms_per_step": round(tt * 1e3, 3), "tflops_effective": round(flop / tt / 1e12, 2),
+                "note": "same BF16 NS with torch.bmm (hipBLASLt), NS steps only, context"}
+        except Exception as exc:   # context only; never fails the bench line
+            bf16["torch_bmm_reference"] = {"error": str(exc)[:200]}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfp4root.so")
-SOURCES = ["quant.hip", "gemm.hip", "api.cpp"]
+SOURCES = ["quant.hip", "gemm_fp4.hip", "gemm_bf16.hip", "api.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -18,9 +18,10 @@ HIPCC_FLAGS = [
     # never emit packed FP32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
-    # MFMA results in VGPRs: the exact product reads every result on the VALU
-    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
+# per-source extra flags: the exact NVFP4 product reads every MFMA result on the
+# VALU, so its MFMA results live in VGPRs; the BF16 product keeps accumulators in AGPRs
+SOURCE_FLAGS = {"gemm_fp4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -39,7 +40,8 @@ def build(verbose: bool = False, jobs: int = 3, extra_flags=(), out: str = LIB) 
     for src in SOURCES:
         obj = os.path.join(objdir, src + ".o")
         objs.append(obj)
-        cmd = [cc, *HIPCC_FLAGS, *extra_flags, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [cc, *HIPCC_FLAGS, *SOURCE_FLAGS.get(src, []), *extra_flags, "-x", "hip", "-c",
+               os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))

@@ -14,9 +14,6 @@
 // exact block sum.  Block sums are accumulated in binary64 and the epilogue
 // forms the output in binary64 and rounds once to binary32, so every product
 // equals the binary32 rounding of its exact value.
-//
-// BF16 operands (comparison path): standard MFMA 32x32x16 bf16 with binary32
-// accumulation across the whole K loop.
 #include "device.h"
 #include "internal.h"
 
@@ -362,173 +359,6 @@ hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st) 
       break;
     default:
       hipLaunchKernelGGL((k_gemm_fp4<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-  }
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// BF16 comparison product: plain MFMA accumulation in binary32.
-
-#ifndef FP4R_BF16_WAVES_M
-#define FP4R_BF16_WAVES_M 4
-#endif
-#ifndef FP4R_BF16_WAVES_N
-#define FP4R_BF16_WAVES_N 2
-#endif
-#ifndef FP4R_BF16_TM
-#define FP4R_BF16_TM 2
-#endif
-#ifndef FP4R_BF16_TN
-#define FP4R_BF16_TN 4
-#endif
-
-template <int ROWS, int NT>
-struct Bf16Stage {
-  static constexpr int kPer = ROWS * 8 / NT;   // 16-byte chunks per thread per stage
-  uint4 v[kPer];
-};
-
-template <int ROWS, int NT>
-FP4R_DEV void bf16_load(const uint16_t* base, int64_t rows, int64_t K, int64_t row0, int stage,
-                        Bf16Stage<ROWS, NT>& s) {
-#pragma unroll
-  for (int q = 0; q < Bf16Stage<ROWS, NT>::kPer; ++q) {
-    const int idx = threadIdx.x + NT * q;
-    const int64_t grow = row0 + (idx >> 3);
-    const int64_t k = (int64_t)stage * KS + (idx & 7) * 8;
-    if (grow < rows && k < K)
-      s.v[q] = *reinterpret_cast<const uint4*>(base + grow * K + k);
-    else
-      s.v[q] = make_uint4(0u, 0u, 0u, 0u);
-  }
-}
-
-template <int ROWS, int NT>
-FP4R_DEV void bf16_store(uint16_t* lds, const Bf16Stage<ROWS, NT>& s) {
-#pragma unroll
-  for (int q = 0; q < Bf16Stage<ROWS, NT>::kPer; ++q) {
-    const int idx = threadIdx.x + NT * q;
-    *reinterpret_cast<uint4*>(lds + lds_idx(idx >> 3, idx & 7)) = s.v[q];
-  }
-}
-
-FP4R_DEV uint16_t to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
-FP4R_DEV float from_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int tiles_m, int tiles_n,
-                                                             int64_t tiles_per_mat) {
-  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
-  __shared__ uint16_t lds_a[2][BM * KS];
-  __shared__ uint16_t lds_b[2][BN * KS];
-  constexpr bool kSym = MODE != kModeUpdateX;
-  const int64_t mat = blockIdx.x / tiles_per_mat;
-  int tm, tn;
-  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
-  const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN_, wn = wave % WN_;
-  const int nstages = (int)((g.K + KS - 1) / KS);
-  const uint16_t* A = g.a + mat * g.a_bstride;
-  const uint16_t* B = g.b + mat * g.b_bstride;
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
-
-  Bf16Stage<BM, NT> sa;
-  Bf16Stage<BN, NT> sb;
-  bf16_load<BM, NT>(A, g.M, g.K, row0, 0, sa);
-  bf16_load<BN, NT>(B, g.N, g.K, col0, 0, sb);
-  bf16_store<BM, NT>(lds_a[0], sa);
-  bf16_store<BN, NT>(lds_b[0], sb);
-  __syncthreads();
-  for (int s = 0; s < nstages; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nstages) {
-      bf16_load<BM, NT>(A, g.M, g.K, row0, s + 1, sa);
-      bf16_load<BN, NT>(B, g.N, g.K, col0, s + 1, sb);
-    }
-    const uint16_t* la = lds_a[buf];
-    const uint16_t* lb = lds_b[buf];
-    const int64_t krem = g.K - (int64_t)s * KS;
-    const int kbs = (int)(krem < KS ? krem / 16 : 4);
-    for (int kb = 0; kb < kbs; ++kb) {
-      const int chunk = kb * 2 + (lane >> 5);
-      bf16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (s + 1 < nstages) {
-      bf16_store<BM, NT>(lds_a[buf ^ 1], sa);
-      bf16_store<BN, NT>(lds_b[buf ^ 1], sb);
-    }
-    __syncthreads();
-  }
-
-  const bool mirror = kSym && tm != tn;
-  uint16_t* o16 = g.out16 + mat * g.out16_bstride;
-  const uint16_t* aux16 = g.aux16 ? g.aux16 + mat * g.out16_bstride : nullptr;
-  float* X = g.x ? g.x + mat * g.x_bstride : nullptr;
-  uint16_t* o16t = g.out16t ? g.out16t + mat * g.out16t_bstride : nullptr;
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t r = row0 + (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int64_t c = col0 + (wn * TN + j) * 32 + (lane & 31);
-        if (r < g.M && c < g.N) {
-          float v = acc[i][j][e];
-          if (MODE == kModeGramB) v = g.cb * from_bf16(aux16[r * g.N + c]) + g.cc * v;
-          if (MODE == kModeUpdateX) {
-            v = g.ca * X[r * g.N + c] + v;
-            X[r * g.N + c] = v;
-            const uint16_t h = to_bf16(v);
-            o16[r * g.N + c] = h;
-            o16t[c * g.M + r] = h;
-          } else {
-            const uint16_t h = to_bf16(v);
-            o16[r * g.N + c] = h;
-            if (mirror) o16[c * g.N + r] = h;
-          }
-        }
-      }
-}
-
-hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st) {
-  constexpr int WM_ = FP4R_BF16_WAVES_M, WN_ = FP4R_BF16_WAVES_N, TM = FP4R_BF16_TM, TN = FP4R_BF16_TN;
-  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
-  static_assert(BM == BN, "symmetric products need square tiles");
-  static_assert((BM * 8) % NT == 0, "each thread stages whole 16-byte chunks");
-  const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
-  const bool sym = mode != kModeUpdateX;
-  const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
-  const dim3 grid((uint32_t)(per * g.batch));
-  switch (mode) {
-    case kModeGramA:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    case kModeGramB:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    default:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
   }
   return hipGetLastError();
 }
