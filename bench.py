@@ -27,6 +27,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+COPY_PROBE_BYTES = 256 << 20
 METRIC = "NS-orthogonalised matrices/s + effective TFLOP/s (% MFMA peak), 3B-shaped set"
 BF16_MFMA_PEAK_TFLOPS = 2516.6
 # VALU ceiling of the exact NVFP4 product: each 16-element block product (16 MACs per
@@ -122,6 +123,9 @@ def main():
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--probe", action="store_true",
+                    help="for hardware-counter runs: one warm and one profiled orthogonalize call, "
+                         "then a plain 256 MiB device copy as the byte-count reference; no timing")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -154,6 +158,15 @@ def main():
     if orth.status() != 0:
         print(json.dumps({"error": f"device status {orth.status()}"}))
         sys.exit(1)
+    if args.probe:
+        orth()
+        src = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"probe": args.case, "copy_bytes": COPY_PROBE_BYTES}), flush=True)
+        return
     t_step = time_calls(orth, args.warmup, args.steps, torch)
     value = len(shapes) / t_step
     tflops = flop / t_step / 1e12

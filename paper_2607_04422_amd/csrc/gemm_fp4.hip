@@ -14,6 +14,22 @@
 // exact block sum.  Block sums are accumulated in binary64 and the epilogue
 // forms the output in binary64 and rounds once to binary32, so every product
 // equals the binary32 rounding of its exact value.
+//
+// Chained blocks.  Element values are q s with q = k/2 (|k| <= 12) and
+// s = M 2^(e-10) (E4M3: M <= 15, e >= 1; subnormal scales as M = m, e = 1), so
+// every product of a row i of the first operand and a row j of the second over
+// a group G of blocks is a multiple of u = 2^(ea_min(i) + eb_min(j) - 22), the
+// minima over G.  By Cauchy-Schwarz, any partial sum of those products is at
+// most |G| sqrt(max_b T_a(i,b) max_b T_b(j,b)) in magnitude, T being a block's
+// sum of squared values.  With rho_i = max_b T_a(i,b) 2^(22 - 2 ea_min(i)) (and
+// sigma_j alike) the bound is below 2^24 u whenever |G|^2 rho_i sigma_j < 2^48;
+// then every partial sum is exactly representable in binary32, and the MFMAs
+// of the group may accumulate into one binary32 register, folded into binary64
+// once.  The loader computes rho per row for the pairs (0,1), (2,3) and the
+// whole 4-block stage, the maximum over its 16 rows goes to LDS, and each
+// compute wave tests the maxima over its own rows (diagonal tiles of symmetric
+// products test tile-wide maxima, so that (i, j) and (j, i) add the same
+// binary32 values in the same order and the product stays exactly symmetric).
 #include "device.h"
 #include "internal.h"
 
@@ -40,9 +56,27 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #define FP4R_FP4_TN 2
 #endif
 constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
+// Chained accumulation of block groups whose exactness bound holds (1) or one
+// binary64 fold per block (0).
+#ifndef FP4R_FP4_CHAIN
+#define FP4R_FP4_CHAIN 1
+#endif
 
-// LDS element (row, k) of a ROWS x 64 16-bit tile: 16-byte chunks XOR-swizzled by row.
-FP4R_DEV int lds_idx(int row, int chunk) { return row * KS + ((chunk ^ (row & 7)) << 3); }
+// LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two 16-byte
+// halves h) of row r at byte
+//   kb_base(kb) + 32 r + 16 (h ^ bit 2 of r),   kb_base(kb) = 32 ROWS kb + {0, 64, 144, 208}[kb].
+// A 16-byte access is served per 8 lanes.  MFMA operand reads (8 consecutive rows,
+// one block and half) then cover all 32 banks, and so do the loader's writes
+// (rows r, r + 1 times the four blocks: the block bases differ by 0, 64, 16 and 80
+// modulo 128 bytes).  The block and buffer offsets are constants, so one address
+// register per operand tile serves every block of both buffers.
+FP4R_DEV int lds_row_off(int row, int h) { return row * 32 + ((h ^ ((row >> 2) & 1)) << 4); }
+template <int ROWS>
+constexpr int lds_kb_base(int kb) {
+  return 32 * ROWS * kb + (kb == 0 ? 0 : kb == 1 ? 64 : kb == 2 ? 144 : 208);
+}
+template <int ROWS>
+constexpr int lds_stage_bytes() { return lds_kb_base<ROWS>(3) + 32 * ROWS; }
 
 // Output tile coordinates.  Symmetric products enumerate the upper triangle
 // row by row; others are row-major over (tiles_m x tiles_n).
@@ -69,28 +103,48 @@ FP4R_DEV void tile_coords(int64_t t, int tiles_m, int tiles_n, bool sym, int& tm
 template <int ROWS, int NT>
 struct Fp4Stage {
   static constexpr int kPer = ROWS * 4 / NT;   // blocks per thread per stage
+  static_assert(kPer == 1, "each thread stages one block of each operand per stage");
   uint2 codes[kPer];
   uint32_t scales[kPer];
 };
 
-template <int ROWS, int NT>
-FP4R_DEV void fp4_load(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t K, int64_t row0,
-                       int stage, Fp4Stage<ROWS, NT>& s) {
+// Where a thread's blocks come from: raw buffer resources over the tile's rows
+// of codes and scales (the hardware range check returns 0 for rows past the
+// matrix, so the tail tile needs no branch) and the thread's byte offsets at
+// stage 0.  Thread t stages row t / 4, block t % 4 of every 64-element stage.
+constexpr int kBufWord3 = 0x00020000;          // raw 32-bit data format, no swizzle
+constexpr uint32_t kBufOutOfRange = 0x7FFFFFF0u;
+
+struct Fp4Src {
+  __amdgpu_buffer_rsrc_t codes, scales;
+  uint32_t oc, os;
+  int kq;
+};
+
+template <int ROWS>
+FP4R_DEV Fp4Src fp4_src(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t K, int64_t row0) {
   const int64_t nkb = K / 16;
-#pragma unroll
-  for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
-    const int idx = threadIdx.x + NT * j;
-    const int r = idx >> 2;
-    const int64_t kb = (int64_t)stage * 4 + (idx & 3);
-    const int64_t grow = row0 + r;
-    if (grow < rows && kb < nkb) {
-      s.codes[j] = *reinterpret_cast<const uint2*>(op.codes + mat * op.codes_bstride + grow * (K / 2) + kb * 8);
-      s.scales[j] = op.scales[mat * op.scales_bstride + grow * nkb + kb];
-    } else {
-      s.codes[j] = make_uint2(0u, 0u);
-      s.scales[j] = 0u;
-    }
-  }
+  const int64_t live = rows - row0 < ROWS ? rows - row0 : ROWS;
+  Fp4Src s;
+  s.codes = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(op.codes + mat * op.codes_bstride + row0 * (K / 2)), (short)0, (int)(live * (K / 2)), kBufWord3);
+  s.scales = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(op.scales + mat * op.scales_bstride + row0 * nkb), (short)0, (int)(live * nkb), kBufWord3);
+  const int r = threadIdx.x >> 2;
+  s.kq = threadIdx.x & 3;
+  s.oc = (uint32_t)(r * (K / 2) + s.kq * 8);
+  s.os = (uint32_t)(r * nkb + s.kq);
+  return s;
+}
+
+template <int ROWS, int NT>
+FP4R_DEV void fp4_load(const Fp4Src& src, int64_t nkb, int stage, Fp4Stage<ROWS, NT>& s) {
+  const bool valid = (int64_t)stage * 4 + src.kq < nkb;   // blocks past the end of K read as 0
+  const uint32_t oc = valid ? src.oc + 32u * (uint32_t)stage : kBufOutOfRange;
+  const uint32_t os = valid ? src.os + 4u * (uint32_t)stage : kBufOutOfRange;
+  const auto c = __builtin_amdgcn_raw_buffer_load_b64(src.codes, (int)oc, 0, 0);
+  s.codes[0] = make_uint2(c[0], c[1]);
+  s.scales[0] = __builtin_amdgcn_raw_buffer_load_b8(src.scales, (int)os, 0, 0);
 }
 
 template <int SEL>
@@ -100,8 +154,59 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
   return q * s2;
 }
 
+// Chain bounds of one staged block group (see the header).  `t` is the thread's
+// block sum of squares; lanes 4r + {0, 1, 2, 3} hold the four blocks of row r.
+// Writes, for the loader wave's 16 rows, max rho of the whole stage, of pair
+// (0,1) and of pair (2,3) (binary32 bit patterns; non-negative values order as
+// unsigned integers) to rec[0], rec[kGroups], rec[2 kGroups].
+template <int CTRL>
+FP4R_DEV uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppSwap1 = 0xB1;     // quad_perm [1, 0, 3, 2]
+constexpr int kDppSwap2 = 0x4E;     // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowRor4 = 0x124;  // rotate right by 4 within 16 lanes
+constexpr int kDppRowRor8 = 0x128;
+
+template <int kGroups>
+FP4R_DEV void fp4_chain_info(uint32_t scale, float t, uint32_t* rec) {
+  const uint32_t sc = scale & 0x7Fu;
+  // a zero block adds nothing to any group and leaves the row's minimum alone
+  const uint32_t e = sc ? max(sc >> 3, 1u) : 15u;
+  const uint32_t e2 = min(e, dpp<kDppSwap1>(e));
+  const uint32_t t2 = max(__float_as_uint(t), dpp<kDppSwap1>(__float_as_uint(t)));
+  const uint32_t e4 = min(e2, dpp<kDppSwap2>(e2));
+  const uint32_t t4 = max(t2, dpp<kDppSwap2>(t2));
+  uint32_t r2 = __float_as_uint(ldexpf(__uint_as_float(t2), 22 - 2 * (int)e2));
+  uint32_t r4 = __float_as_uint(ldexpf(__uint_as_float(t4), 22 - 2 * (int)e4));
+  r2 = max(r2, dpp<kDppRowRor4>(r2));
+  r2 = max(r2, dpp<kDppRowRor8>(r2));
+  r4 = max(r4, dpp<kDppRowRor4>(r4));
+  r4 = max(r4, dpp<kDppRowRor8>(r4));
+  auto lanes_max = [](uint32_t v, int l) {
+    return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, l), (uint32_t)__builtin_amdgcn_readlane((int)v, l + 16)),
+               max((uint32_t)__builtin_amdgcn_readlane((int)v, l + 32), (uint32_t)__builtin_amdgcn_readlane((int)v, l + 48)));
+  };
+  const uint32_t q = lanes_max(r4, 0), p0 = lanes_max(r2, 0), p1 = lanes_max(r2, 2);
+  if ((threadIdx.x & 63) == 0) {
+    rec[0] = q;
+    rec[kGroups] = p0;
+    rec[2 * kGroups] = p1;
+  }
+}
+
+// Largest of n records from g0 (wave-uniform), as binary32.
+FP4R_DEV float rho_max(const uint32_t* rec, int g0, int n) {
+  uint32_t m = 0;
+  for (int g = 0; g < n; ++g) m = max(m, rec[g0 + g]);
+  return __uint_as_float(m);
+}
+
+// Decodes the staged blocks into the LDS stage at `lds`; returns the (exact) sum
+// of squares of the thread's 16 decoded values.
 template <int ROWS, int NT>
-FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage<ROWS, NT>& s) {
+FP4R_DEV float fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
+  float t = 0.0f;
 #pragma unroll
   for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
     const int idx = threadIdx.x + NT * j;
@@ -111,14 +216,24 @@ FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage<ROWS, NT>& s) {
     const uint32_t w[2] = {s.codes[j].x, s.codes[j].y};
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      f16x8 v;
       const f16x2 p0 = fp4_pair<0>(w[half], s2), p1 = fp4_pair<1>(w[half], s2);
       const f16x2 p2 = fp4_pair<2>(w[half], s2), p3 = fp4_pair<3>(w[half], s2);
+      f16x8 v;
       v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
-      *reinterpret_cast<f16x8*>(lds + lds_idx(r, kb * 2 + half)) = v;
+      const int kbo = kb == 0 ? lds_kb_base<ROWS>(0) : kb == 1 ? lds_kb_base<ROWS>(1)
+                    : kb == 2 ? lds_kb_base<ROWS>(2) : lds_kb_base<ROWS>(3);
+      *reinterpret_cast<f16x8*>(lds + kbo + lds_row_off(r, half)) = v;
+#if FP4R_FP4_CHAIN
+      // squares of values with at most 6 significant bits: every partial sum is exact
+      t = __builtin_amdgcn_fdot2(p0, p0, t, false);
+      t = __builtin_amdgcn_fdot2(p1, p1, t, false);
+      t = __builtin_amdgcn_fdot2(p2, p2, t, false);
+      t = __builtin_amdgcn_fdot2(p3, p3, t, false);
+#endif
     }
   }
+  return t;
 }
 
 // ---------------------------------------------------------------------------
@@ -127,8 +242,9 @@ FP4R_DEV void fp4_store(_Float16* lds, const Fp4Stage<ROWS, NT>& s) {
 #ifndef FP4R_FP4_WAVES_PER_EU
 #define FP4R_FP4_WAVES_PER_EU 4
 #endif
-#ifndef FP4R_FP4_PIPELINE
-#define FP4R_FP4_PIPELINE 0
+// Stages in flight in registers ahead of the one in LDS (1 or 2).
+#ifndef FP4R_FP4_PREFETCH
+#define FP4R_FP4_PREFETCH 1
 #endif
 
 template <int MODE, int WM_, int WN_, int TM, int TN>
@@ -136,11 +252,18 @@ __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(F
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) {
   constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
   constexpr int kLdT = BN + 1;   // padded row of the FP32 output tile staged in LDS
-  constexpr size_t kMainBytes = (size_t)2 * (BM + BN) * KS * sizeof(_Float16);
+  constexpr int kStA = lds_stage_bytes<BM>(), kStB = lds_stage_bytes<BN>();
+  constexpr size_t kMainBytes = (size_t)2 * (kStA + kStB);
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
-  __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
-  _Float16(*lds_a)[BM * KS] = reinterpret_cast<_Float16(*)[BM * KS]>(smem);
-  _Float16(*lds_b)[BN * KS] = reinterpret_cast<_Float16(*)[BN * KS]>(smem + 2 * BM * KS * sizeof(_Float16));
+  constexpr int kGa = BM / 16, kGb = BN / 16;   // loader groups (16 rows) per operand tile
+  // chain records per buffer: [operand][stage, pair 0, pair 1][loader group]
+  constexpr int kRec = 3 * (kGa + kGb);
+  constexpr size_t kRecBytes = FP4R_FP4_CHAIN ? (size_t)2 * kRec * sizeof(uint32_t) : 0;
+  constexpr size_t kLoopBytes = kMainBytes + kRecBytes;
+  __shared__ __attribute__((aligned(16))) char smem[kLoopBytes > kEpiBytes ? kLoopBytes : kEpiBytes];
+  uint32_t(*crec)[kRec] = reinterpret_cast<uint32_t(*)[kRec]>(smem + kMainBytes);
+  char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
+  char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
   constexpr bool kSym = MODE != kModeUpdateX;
   const int64_t mat = blockIdx.x / tiles_per_mat;
   int tm, tn;
@@ -159,80 +282,96 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0;
 
-  Fp4Stage<BM, NT> sa;
-  Fp4Stage<BN, NT> sb;
-  fp4_load<BM, NT>(g.a, mat, g.M, g.K, row0, 0, sa);
-  fp4_load<BN, NT>(g.b, mat, g.N, g.K, col0, 0, sb);
-  fp4_store<BM, NT>(lds_a[0], sa);
-  fp4_store<BN, NT>(lds_b[0], sb);
-  __syncthreads();
+  const Fp4Src src_a = fp4_src<BM>(g.a, mat, g.M, g.K, row0);
+  const Fp4Src src_b = fp4_src<BN>(g.b, mat, g.N, g.K, col0);
+#if FP4R_FP4_CHAIN
+  static_assert(kGa == kGb, "square tiles");
+  // the rows a compute wave covers: TM * 2 loader groups of A, TN * 2 of B;
+  // diagonal tiles of symmetric products use all groups (see the header)
+  const int uwave = __builtin_amdgcn_readfirstlane(wave);
+  const bool diag = kSym && tm == tn;
+  const int ga0 = diag ? 0 : (uwave / WN_) * TM * 2, nga = diag ? kGa : TM * 2;
+  const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
+  // a stage chains as one group if 16 rho sigma < 2^48, a pair if 4 rho sigma < 2^48;
+  // the limits leave room for the rounding of the binary32 product rho * sigma
+  constexpr float kLimStage = 17592186044416.0f * (1.0f - 1.0f / 65536.0f);   // 2^44 (1 - 2^-16)
+  constexpr float kLimPair = 70368744177664.0f * (1.0f - 1.0f / 65536.0f);    // 2^46 (1 - 2^-16)
+#endif
+
+  // stage -> LDS buffer `buf` (decoded operands and chain records)
+  auto put = [&](int buf, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) {
+    const float ta = fp4_store<BM, NT>(lds_a[buf], xa);
+    const float tb = fp4_store<BN, NT>(lds_b[buf], xb);
+#if FP4R_FP4_CHAIN
+    fp4_chain_info<kGa>(xa.scales[0], ta, crec[buf] + wave);
+    fp4_chain_info<kGb>(xb.scales[0], tb, crec[buf] + 3 * kGa + wave);
+#else
+    (void)ta;
+    (void)tb;
+#endif
+  };
 
   const f32x16 zero = {};
-  for (int s = 0; s < nstages; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nstages) {
-      fp4_load<BM, NT>(g.a, mat, g.M, g.K, row0, s + 1, sa);
-      fp4_load<BN, NT>(g.b, mat, g.N, g.K, col0, s + 1, sb);
-    }
-    const _Float16* la = lds_a[buf];
-    const _Float16* lb = lds_b[buf];
-    const int kbs = (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4);
-#if FP4R_FP4_PIPELINE
-    // Software pipeline over the stage's (block, tile) jobs: the MFMA of job t+1
-    // is in flight while the block sums of job t are folded into binary64.
-    {
-      constexpr int kJobs = TM * TN;
-      f16x8 af[TM], bfr[TN];
-      f32x16 pend;
-      int pend_i = 0, pend_j = 0;
-      bool have = false;
-      for (int kb = 0; kb < kbs; ++kb) {
-        const int chunk = kb * 2 + (lane >> 5);
+  // MFMAs and binary64 folds of the stage in LDS buffer `buf` (kbs blocks)
+  auto compute = [&](int buf, int kbs) {
+    if (kbs <= 0) return;
+    const char* la = lds_a[buf];
+    const char* lb = lds_b[buf];
+#if FP4R_FP4_CHAIN
+    // chain flags: bit k - 1 set = block k accumulates onto block k - 1 (blocks
+    // past the end of K are zero in LDS and join any group)
+    const uint32_t* ra = crec[buf];
+    const uint32_t* rb = crec[buf] + 3 * kGa;
+    const float st = rho_max(ra, ga0, nga) * rho_max(rb, gb0, ngb);
+    const float p0 = rho_max(ra + kGa, ga0, nga) * rho_max(rb + kGb, gb0, ngb);
+    const float p1 = rho_max(ra + 2 * kGa, ga0, nga) * rho_max(rb + 2 * kGb, gb0, ngb);
+    const uint32_t fl = __builtin_amdgcn_readfirstlane(
+        st < kLimStage ? 7u : ((p0 < kLimPair ? 1u : 0u) | (p1 < kLimPair ? 4u : 0u)));
+    // the TM x TN tiles' chains run interleaved, block by block
+    f32x16 p[TM][TN];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
+    for (int kb = 0; kb < 4; ++kb) {
+      f16x8 av[TM], bv[TN];
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
+      for (int i = 0; i < TM; ++i)
+        av[i] = *reinterpret_cast<const f16x8*>(
+            la + lds_kb_base<BM>(kb) + lds_row_off((wm * TM + i) * 32 + (lane & 31), lane >> 5));
 #pragma unroll
-        for (int t = 0; t < kJobs; ++t) {
-          const int i = t / TN, j = t % TN;
-          const f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
-          if (have) {
+      for (int j = 0; j < TN; ++j)
+        bv[j] = *reinterpret_cast<const f16x8*>(
+            lb + lds_kb_base<BN>(kb) + lds_row_off((wn * TN + j) * 32 + (lane & 31), lane >> 5));
+      const bool chained = kb > 0 && ((fl >> (kb - 1)) & 1u);
 #pragma unroll
-            for (int ii = 0; ii < TM; ++ii)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-              for (int jj = 0; jj < TN; ++jj)
-                if (ii == pend_i && jj == pend_j)
+        for (int j = 0; j < TN; ++j) {
+          if (kb > 0 && !chained) {
 #pragma unroll
-                  for (int e = 0; e < 16; ++e) acc[ii][jj][e] = acc[ii][jj][e] + (double)pend[e];
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
           }
-          pend = p;
-          pend_i = i;
-          pend_j = j;
-          have = true;
+          p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], chained ? p[i][j] : zero, 0, 0, 0);
         }
-      }
-      if (have) {
-#pragma unroll
-        for (int ii = 0; ii < TM; ++ii)
-#pragma unroll
-          for (int jj = 0; jj < TN; ++jj)
-            if (ii == pend_i && jj == pend_j)
-#pragma unroll
-              for (int e = 0; e < 16; ++e) acc[ii][jj][e] = acc[ii][jj][e] + (double)pend[e];
-      }
+      __builtin_amdgcn_sched_barrier(0);   // keep operand loads next to their use
     }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
 #else
-    for (int kb = 0; kb < kbs; ++kb) {
-      const int chunk = kb * 2 + (lane >> 5);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      if (kb >= kbs) break;
       f16x8 af[TM], bfr[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const f16x8*>(la + lds_idx((wm * TM + i) * 32 + (lane & 31), chunk));
+        af[i] = *reinterpret_cast<const f16x8*>(
+            la + lds_kb_base<BM>(kb) + lds_row_off((wm * TM + i) * 32 + (lane & 31), lane >> 5));
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const f16x8*>(lb + lds_idx((wn * TN + j) * 32 + (lane & 31), chunk));
+        bfr[j] = *reinterpret_cast<const f16x8*>(
+            lb + lds_kb_base<BN>(kb) + lds_row_off((wn * TN + j) * 32 + (lane & 31), lane >> 5));
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -243,12 +382,49 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
         }
     }
 #endif
-    if (s + 1 < nstages) {
-      fp4_store<BM, NT>(lds_a[buf ^ 1], sa);
-      fp4_store<BN, NT>(lds_b[buf ^ 1], sb);
-    }
+  };
+  auto blocks_in = [&](int s) { return (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4); };
+
+  Fp4Stage<BM, NT> sa, na;
+  Fp4Stage<BN, NT> sb, nb;
+  fp4_load<BM, NT>(src_a, nkb, 0, sa);
+  fp4_load<BN, NT>(src_b, nkb, 0, sb);
+  put(0, sa, sb);
+#if FP4R_FP4_PREFETCH == 2
+  // Stage s is computed from LDS while stage s + 1 waits in one register set and
+  // stage s + 2 loads into the other; the loop body runs two stages with the
+  // sets swapped, so no register copy waits on a load in flight.
+  fp4_load<BM, NT>(src_a, nkb, 1, sa);
+  fp4_load<BN, NT>(src_b, nkb, 1, sb);
+  __syncthreads();
+  auto step = [&](int s, int buf, Fp4Stage<BM, NT>& ha, Fp4Stage<BN, NT>& hb, Fp4Stage<BM, NT>& la2,
+                  Fp4Stage<BN, NT>& lb2) {
+    // unconditional: past the last stage every offset is out of range and reads 0,
+    // and a branch here would make the waits below cover these loads too
+    fp4_load<BM, NT>(src_a, nkb, s + 2, la2);
+    fp4_load<BN, NT>(src_b, nkb, s + 2, lb2);
+    compute(buf, blocks_in(s));
+    put(buf ^ 1, ha, hb);
+    __syncthreads();
+  };
+  // no data-dependent branch in the loop body (a stage past the end computes
+  // nothing and stages zeros), so the load waits stay exact
+  for (int s = 0; s < nstages; s += 2) {
+    step(s, 0, sa, sb, na, nb);
+    step(s + 1, 1, na, nb, sa, sb);
+  }
+#else
+  __syncthreads();
+  for (int s = 0; s < nstages; ++s) {
+    fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
+    fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
+    compute(s & 1, blocks_in(s));
+    put((s & 1) ^ 1, sa, sb);
     __syncthreads();
   }
+  (void)na;
+  (void)nb;
+#endif
 
   // epilogue: binary64 formula, one rounding to binary32, staged through LDS
   // (the main loop's buffers are free after the last barrier)
@@ -258,6 +434,25 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   float* out = g.out + mat * g.out_bstride;
   const float* aux = g.aux ? g.aux + mat * g.out_bstride : nullptr;
   float* tile = reinterpret_cast<float*>(smem);
+  // the epilogue operand (A for B, X_k for X_{k+1}) of all of this lane's
+  // outputs, loaded up front (in-range index for lanes past the edge)
+  float xin[TM][TN][16];
+  if (MODE != kModeGramA) {
+    const int64_t live = g.M - row0 < BM ? g.M - row0 : BM;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(aux + row0 * g.N), (short)0, (int)(live * g.N * 4), kBufWord3);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int rl = (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          const int64_t c = col0 + (wn * TN + j) * 32 + (lane & 31);
+          const uint32_t off = c < g.N ? (uint32_t)((rl * g.N + c) * 4) : kBufOutOfRange;
+          xin[i][j][e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)off, 0, 0));
+        }
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -266,15 +461,11 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
       for (int e = 0; e < 16; ++e) {
         const int rl = (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         const int cl = (wn * TN + j) * 32 + (lane & 31);
-        const int64_t r = row0 + rl, c = col0 + cl;
-        float f = 0.0f;
-        if (r < g.M && c < g.N) {
-          double v = alpha * acc[i][j][e];
-          if (MODE == kModeGramB) v = cb * (double)aux[r * g.N + c] + cc * v;
-          if (MODE == kModeUpdateX) v = ca * (double)aux[r * g.N + c] + v;
-          f = (float)v;
-        }
-        tile[rl * kLdT + cl] = f;
+        double v = alpha * acc[i][j][e];
+        if (MODE == kModeGramB) v = cb * (double)xin[i][j][e] + cc * v;
+        if (MODE == kModeUpdateX) v = ca * (double)xin[i][j][e] + v;
+        const bool in = row0 + rl < g.M && col0 + cl < g.N;
+        tile[rl * kLdT + cl] = in ? (float)v : 0.0f;
       }
   __syncthreads();
   // coalesced stores: rows of the tile, and (off-diagonal symmetric tiles) its transpose

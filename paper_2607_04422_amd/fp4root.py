@@ -53,11 +53,13 @@ class NsTrace(ctypes.Structure):
 _lib = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load the library (once).  Raises if it has not been built."""
+def load(path: str = None) -> ctypes.CDLL:
+    """Load the library (once): `path`, else $FP4ROOT_LIBRARY, else the in-tree build.
+    Raises if it has not been built."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("FP4ROOT_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"libfp4root.so not built at {path}; run __graft_entry__.build()")
     lib = ctypes.CDLL(path)

@@ -81,6 +81,12 @@ def test_argument_errors_are_synchronous():
     assert lib.fp4root_ns_step(fake, 1, 64, 64, 4096, nan, 0.0, 0.0, 6, 0, 0, None, ws, 1 << 30, None) == -1
     assert lib.fp4root_ns_step(fake, 1, 64, 72, 4608, 1.0, 0.0, 0.0, 6, 0, 0, None, ws, 1 << 30, None) == -2
     assert lib.fp4root_ns_step(fake, 1, 64, 64, 4096, 1.0, 0.0, 0.0, 6, 0, 0, None, ws, 16, None) == -3
+    # a side above 2^21 (products address 128-row tiles with 32-bit byte offsets)
+    big = (1 << 21) + 16
+    assert lib.fp4root_ns_step(fake, 1, 64, big, 64 * big, 1.0, 0.0, 0.0, 6, 0, 0, None, ws, 1 << 30,
+                               None) == -2
+    assert lib.fp4root_quantize(fake, 1, 64, big, big, 64 * big, 1, 0, 0.99, 0, 0, fake, fake, fake, None,
+                                ws, 1 << 40, None) == -2
     # orthogonalize: unaligned pointer, in-place with different ld, bad count
     cfg = F.NsConfig(5, None, 7, 0.99, 1e-7, 0)
     m1 = (F.Matrix * 1)(F.Matrix(0x100004, 0x300000, 64, 64, 64, 64))
