@@ -30,11 +30,12 @@ sys.path.insert(0, ROOT)
 COPY_PROBE_BYTES = 256 << 20
 METRIC = "NS-orthogonalised matrices/s + effective TFLOP/s (% MFMA peak), 3B-shaped set"
 BF16_MFMA_PEAK_TFLOPS = 2516.6
-# VALU ceiling of the exact NVFP4 product: each 16-element block product (16 MACs per
-# output) is folded into a binary64 accumulator with one conversion and one add, two
-# wave64 VALU instructions per output and block.  256 CUs x 4 SIMDs x 16 lanes x
-# 2.4 GHz = 39.3 T lane-ops/s -> 19.66 T output-blocks/s x 32 FLOP = 629 TFLOP/s.
-EXACT_PRODUCT_ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2.4e9 / 2 * 32 / 1e12
+# The exact NVFP4 products run on the f16 MFMA (32x32x16, decoded operands), whose dense
+# peak is the bf16/fp16 one: 2.5 PFLOP/s.  With whole 4-block stages chained into one
+# binary32 accumulator, the binary64 folds (2 VALU ops per output per 64-element stage)
+# match that rate too: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz / 2 x 128 FLOP = 2516 TFLOP/s.
+F16_MFMA_PEAK_TFLOPS = BF16_MFMA_PEAK_TFLOPS
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_gemm_fp4_update_block3b_x4_traffic.md")
 
 
 def ns_flop(m: int, n: int, steps: int) -> float:
@@ -183,11 +184,15 @@ def main():
         F.fp4root_timer_reset()
         ms2, n2, fl2 = per_kernel[2]            # the update product X <- a X + qB qXt^T
         achieved = fl2 / (ms2 / 1e3) / 1e12 if ms2 > 0 else 0.0
-        peak = EXACT_PRODUCT_ALU_PEAK_TFLOPS
+        peak = F16_MFMA_PEAK_TFLOPS
+        from paper_2607_04422_amd import prof
+        traffic = prof.read_update_traffic(TRAFFIC_RECORD) if args.case == "block3b_x4" else None
         roofline = {
-            "kernel": "k_gemm_fp4<update X> (exact NVFP4 product, f16 MFMA per block, f64 accumulation)",
-            "bound": "alu", "achieved": round(achieved, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "kernel": "k_gemm_fp4<update X> (exact NVFP4 product: f16 MFMA, chained block groups, "
+                      "f64 accumulation)",
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": round(traffic) if traffic is not None else None,
             "avg_launch_ms": round(ms2 / max(n2, 1), 4), "launches": n2,
             "all_products_tflops": round(sum(v[2] for v in per_kernel.values()) /
                                          (sum(v[0] for v in per_kernel.values()) / 1e3) / 1e12, 2),

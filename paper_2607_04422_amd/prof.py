@@ -1,0 +1,146 @@
+"""Summaries of rocprofv3 output for the product kernels (text for a profile record).
+
+    python -m paper_2607_04422_amd.prof stats DIR            kernel-time table from a
+        ``rocprofv3 --kernel-trace --stats --output-format csv -d DIR`` run
+    python -m paper_2607_04422_amd.prof traffic FETCH_DIR WRITE_DIR
+        HBM bytes per launch of each kernel from two ``--pmc FETCH_SIZE`` /
+        ``--pmc WRITE_SIZE`` runs of ``bench.py --probe``, each counter scaled by
+        what it reads for the plain device copy that run ends with
+
+The traffic record carries the SHA-256 of the NVFP4 product source, so that a
+reader (bench.py) can tell whether it still describes the kernel in the tree.
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import glob
+import hashlib
+import os
+import re
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GEMM_SOURCE = os.path.join(HERE, "csrc", "gemm_fp4.hip")
+COPY_KERNEL = "copyBuffer"
+
+
+def source_sha256(path: str = GEMM_SOURCE) -> str:
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def short_name(name: str) -> str:
+    """`void fp4r::k_gemm_fp4<2, 4, 2, 1, 2>(...)` -> `fp4r::k_gemm_fp4<2, 4, 2, 1, 2>`."""
+    name = name.strip().strip('"')
+    if name.startswith("void "):
+        name = name[5:]
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
+
+
+def _one(pattern: str) -> str:
+    hits = sorted(glob.glob(pattern))
+    if not hits:
+        raise FileNotFoundError(pattern)
+    return hits[0]
+
+
+def stats(directory: str):
+    """[(kernel, calls, total_us, average_us, percent)] from a --stats csv, largest first."""
+    path = _one(os.path.join(directory, "*kernel_stats.csv"))
+    rows = []
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            rows.append((short_name(r["Name"]), int(r["Calls"]), float(r["TotalDurationNs"]) / 1e3,
+                         float(r["AverageNs"]) / 1e3, float(r["Percentage"])))
+    return sorted(rows, key=lambda t: -t[2])
+
+
+def per_dispatch(directory: str, counter: str):
+    """{kernel: [value per dispatch]} (KiB for FETCH_SIZE / WRITE_SIZE)."""
+    path = _one(os.path.join(directory, "*counter_collection.csv"))
+    out = collections.OrderedDict()
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            out.setdefault(short_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+    return out
+
+
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int):
+    """Per kernel: mean KiB per dispatch of both counters and calibrated bytes per launch."""
+    fe = per_dispatch(fetch_dir, "FETCH_SIZE")
+    wr = per_dispatch(write_dir, "WRITE_SIZE")
+    copy_f = sum(sum(v) for k, v in fe.items() if COPY_KERNEL in k) * 1024.0
+    copy_w = sum(sum(v) for k, v in wr.items() if COPY_KERNEL in k) * 1024.0
+    if copy_f <= 0 or copy_w <= 0:
+        raise ValueError("no copy-kernel dispatch in the counter runs")
+    kf, kw = copy_bytes / copy_f, copy_bytes / copy_w
+    rows = []
+    for k in fe:
+        if k not in wr or COPY_KERNEL in k:
+            continue
+        f = sum(fe[k]) / len(fe[k])
+        w = sum(wr[k]) / len(wr[k])
+        rows.append((k, len(fe[k]), f, w, (f * kf + w * kw) * 1024.0))
+    return kf, kw, rows
+
+
+def _stats_md(directory: str) -> str:
+    lines = ["| kernel | calls | total us | average us | % |", "|---|---|---|---|---|"]
+    for k, n, tot, avg, pct in stats(directory):
+        lines.append(f"| `{k}` | {n} | {tot:.1f} | {avg:.1f} | {pct:.2f} |")
+    return "\n".join(lines)
+
+
+def _traffic_md(fetch_dir: str, write_dir: str, copy_bytes: int) -> str:
+    kf, kw, rows = traffic(fetch_dir, write_dir, copy_bytes)
+    lines = [f"calibration: plain copy of {copy_bytes} bytes; FETCH_SIZE factor {kf:.4f}, "
+             f"WRITE_SIZE factor {kw:.4f}", "",
+             "| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | HBM bytes/launch (calibrated) |",
+             "|---|---|---|---|---|"]
+    for k, n, f, w, b in rows:
+        lines.append(f"| `{k}` | {n} | {f:.1f} | {w:.1f} | {b:.4g} |")
+    upd = [r for r in rows if r[0].startswith("fp4r::k_gemm_fp4<2")]
+    if upd:
+        lines += ["", f"update_product_traffic_bytes_per_launch: {upd[0][4]:.6g}",
+                  f"gemm_fp4_source_sha256: {source_sha256()}"]
+    return "\n".join(lines)
+
+
+def read_update_traffic(path: str):
+    """Bytes per launch of the update product from a traffic record, or None when the
+    record is missing or was taken from a different version of the product source."""
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"update_product_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    h = re.search(r"gemm_fp4_source_sha256:\s*([0-9a-f]{64})", text)
+    if not m or not h or h.group(1) != source_sha256():
+        return None
+    return float(m.group(1))
+
+
+def main(argv):
+    if len(argv) >= 2 and argv[0] == "stats":
+        print(_stats_md(argv[1]))
+    elif len(argv) >= 3 and argv[0] == "traffic":
+        copy_bytes = int(argv[3]) if len(argv) > 3 else 256 << 20
+        print(_traffic_md(argv[1], argv[2], copy_bytes))
+    else:
+        print(__doc__)
+        return 2
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1:]))
