@@ -25,8 +25,8 @@
 // sigma_j alike) the bound is below 2^24 u whenever |G|^2 rho_i sigma_j < 2^48;
 // then every partial sum is exactly representable in binary32, and the MFMAs
 // of the group may accumulate into one binary32 register, folded into binary64
-// once.  The loader computes rho per row for the pairs (0,1), (2,3) and the
-// whole 4-block stage, the maximum over its 16 rows goes to LDS, and each
+// once.  The loader computes rho per row for the whole 4-block stage, the
+// maximum over its 16 rows goes to LDS, and each
 // compute wave tests the maxima over its own rows (diagonal tiles of symmetric
 // products test tile-wide maxima, so that (i, j) and (j, i) add the same
 // binary32 values in the same order and the product stays exactly symmetric).
@@ -77,6 +77,8 @@ constexpr int lds_kb_base(int kb) {
 }
 template <int ROWS>
 constexpr int lds_stage_bytes() { return lds_kb_base<ROWS>(3) + 32 * ROWS; }
+static_assert(lds_kb_base<128>(2) == 32 * 128 * 2 + 64 * 2 + 16 && lds_kb_base<128>(3) == 32 * 128 * 3 + 64 * 3 + 16,
+              "block bases");
 
 // Output tile coordinates.  Symmetric products enumerate the upper triangle
 // row by row; others are row-major over (tiles_m x tiles_n).
@@ -154,11 +156,10 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
   return q * s2;
 }
 
-// Chain bounds of one staged block group (see the header).  `t` is the thread's
-// block sum of squares; lanes 4r + {0, 1, 2, 3} hold the four blocks of row r.
-// Writes, for the loader wave's 16 rows, max rho of the whole stage, of pair
-// (0,1) and of pair (2,3) (binary32 bit patterns; non-negative values order as
-// unsigned integers) to rec[0], rec[kGroups], rec[2 kGroups].
+// Chain bound of one stage (see the header).  `t` is the thread's block sum of
+// squares; lanes 4r + {0, 1, 2, 3} hold the four blocks of row r.  Writes max
+// rho over the loader wave's 16 rows (binary32 bit pattern; non-negative values
+// order as unsigned integers) to *rec.
 template <int CTRL>
 FP4R_DEV uint32_t dpp(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
@@ -167,8 +168,19 @@ constexpr int kDppSwap1 = 0xB1;     // quad_perm [1, 0, 3, 2]
 constexpr int kDppSwap2 = 0x4E;     // quad_perm [2, 3, 0, 1]
 constexpr int kDppRowRor4 = 0x124;  // rotate right by 4 within 16 lanes
 constexpr int kDppRowRor8 = 0x128;
+constexpr int kDppRowBcast15 = 0x142;   // lane 15 of each row to the next row
+constexpr int kDppRowBcast31 = 0x143;   // lane 31 to rows 2 and 3
 
-template <int kGroups>
+// Largest value over the wave, in lane 63 (non-negative binary32 bit patterns;
+// lanes a broadcast does not write read 0, which leaves the maximum alone).
+FP4R_DEV uint32_t wave_max_to_lane63(uint32_t v) {
+  v = max(v, dpp<kDppRowRor4>(v));
+  v = max(v, dpp<kDppRowRor8>(v));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppRowBcast15, 0xA, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppRowBcast31, 0xC, 0xF, false));
+  return v;
+}
+
 FP4R_DEV void fp4_chain_info(uint32_t scale, float t, uint32_t* rec) {
   const uint32_t sc = scale & 0x7Fu;
   // a zero block adds nothing to any group and leaves the row's minimum alone
@@ -177,22 +189,8 @@ FP4R_DEV void fp4_chain_info(uint32_t scale, float t, uint32_t* rec) {
   const uint32_t t2 = max(__float_as_uint(t), dpp<kDppSwap1>(__float_as_uint(t)));
   const uint32_t e4 = min(e2, dpp<kDppSwap2>(e2));
   const uint32_t t4 = max(t2, dpp<kDppSwap2>(t2));
-  uint32_t r2 = __float_as_uint(ldexpf(__uint_as_float(t2), 22 - 2 * (int)e2));
-  uint32_t r4 = __float_as_uint(ldexpf(__uint_as_float(t4), 22 - 2 * (int)e4));
-  r2 = max(r2, dpp<kDppRowRor4>(r2));
-  r2 = max(r2, dpp<kDppRowRor8>(r2));
-  r4 = max(r4, dpp<kDppRowRor4>(r4));
-  r4 = max(r4, dpp<kDppRowRor8>(r4));
-  auto lanes_max = [](uint32_t v, int l) {
-    return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, l), (uint32_t)__builtin_amdgcn_readlane((int)v, l + 16)),
-               max((uint32_t)__builtin_amdgcn_readlane((int)v, l + 32), (uint32_t)__builtin_amdgcn_readlane((int)v, l + 48)));
-  };
-  const uint32_t q = lanes_max(r4, 0), p0 = lanes_max(r2, 0), p1 = lanes_max(r2, 2);
-  if ((threadIdx.x & 63) == 0) {
-    rec[0] = q;
-    rec[kGroups] = p0;
-    rec[2 * kGroups] = p1;
-  }
+  const uint32_t r4 = wave_max_to_lane63(__float_as_uint(ldexpf(__uint_as_float(t4), 22 - 2 * (int)e4)));
+  if ((threadIdx.x & 63) == 63) *rec = r4;
 }
 
 // Largest of n records from g0 (wave-uniform), as binary32.
@@ -211,8 +209,8 @@ FP4R_DEV float fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
   for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
     const int idx = threadIdx.x + NT * j;
     const int r = idx >> 2, kb = idx & 3;
-    const _Float16 sv = (_Float16)e4m3_value(s.scales[j]);
-    const f16x2 s2 = {sv, sv};
+    // the E4M3 scale in both halves, converted exactly (every E4M3 value is an f16)
+    const f16x2 s2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8((s.scales[j] & 0xFFu) * 0x0101u, 1.0f, false);
     const uint32_t w[2] = {s.codes[j].x, s.codes[j].y};
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -221,8 +219,7 @@ FP4R_DEV float fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
       f16x8 v;
       v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
-      const int kbo = kb == 0 ? lds_kb_base<ROWS>(0) : kb == 1 ? lds_kb_base<ROWS>(1)
-                    : kb == 2 ? lds_kb_base<ROWS>(2) : lds_kb_base<ROWS>(3);
+      const int kbo = 32 * ROWS * kb + 64 * kb + 16 * (kb >> 1);   // lds_kb_base<ROWS>(kb)
       *reinterpret_cast<f16x8*>(lds + kbo + lds_row_off(r, half)) = v;
 #if FP4R_FP4_CHAIN
       // squares of values with at most 6 significant bits: every partial sum is exact
@@ -256,8 +253,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   constexpr size_t kMainBytes = (size_t)2 * (kStA + kStB);
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
   constexpr int kGa = BM / 16, kGb = BN / 16;   // loader groups (16 rows) per operand tile
-  // chain records per buffer: [operand][stage, pair 0, pair 1][loader group]
-  constexpr int kRec = 3 * (kGa + kGb);
+  // chain records per buffer: [A loader groups][B loader groups]
+  constexpr int kRec = kGa + kGb;
   constexpr size_t kRecBytes = FP4R_FP4_CHAIN ? (size_t)2 * kRec * sizeof(uint32_t) : 0;
   constexpr size_t kLoopBytes = kMainBytes + kRecBytes;
   __shared__ __attribute__((aligned(16))) char smem[kLoopBytes > kEpiBytes ? kLoopBytes : kEpiBytes];
@@ -292,10 +289,9 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   const bool diag = kSym && tm == tn;
   const int ga0 = diag ? 0 : (uwave / WN_) * TM * 2, nga = diag ? kGa : TM * 2;
   const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
-  // a stage chains as one group if 16 rho sigma < 2^48, a pair if 4 rho sigma < 2^48;
-  // the limits leave room for the rounding of the binary32 product rho * sigma
+  // a stage chains as one group if 16 rho sigma < 2^48; the limit leaves room
+  // for the rounding of the binary32 product rho * sigma
   constexpr float kLimStage = 17592186044416.0f * (1.0f - 1.0f / 65536.0f);   // 2^44 (1 - 2^-16)
-  constexpr float kLimPair = 70368744177664.0f * (1.0f - 1.0f / 65536.0f);    // 2^46 (1 - 2^-16)
 #endif
 
   // stage -> LDS buffer `buf` (decoded operands and chain records)
@@ -303,8 +299,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     const float ta = fp4_store<BM, NT>(lds_a[buf], xa);
     const float tb = fp4_store<BN, NT>(lds_b[buf], xb);
 #if FP4R_FP4_CHAIN
-    fp4_chain_info<kGa>(xa.scales[0], ta, crec[buf] + wave);
-    fp4_chain_info<kGb>(xb.scales[0], tb, crec[buf] + 3 * kGa + wave);
+    fp4_chain_info(xa.scales[0], ta, crec[buf] + wave);
+    fp4_chain_info(xb.scales[0], tb, crec[buf] + kGa + wave);
 #else
     (void)ta;
     (void)tb;
@@ -320,13 +316,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 #if FP4R_FP4_CHAIN
     // chain flags: bit k - 1 set = block k accumulates onto block k - 1 (blocks
     // past the end of K are zero in LDS and join any group)
-    const uint32_t* ra = crec[buf];
-    const uint32_t* rb = crec[buf] + 3 * kGa;
-    const float st = rho_max(ra, ga0, nga) * rho_max(rb, gb0, ngb);
-    const float p0 = rho_max(ra + kGa, ga0, nga) * rho_max(rb + kGb, gb0, ngb);
-    const float p1 = rho_max(ra + 2 * kGa, ga0, nga) * rho_max(rb + 2 * kGb, gb0, ngb);
-    const uint32_t fl = __builtin_amdgcn_readfirstlane(
-        st < kLimStage ? 7u : ((p0 < kLimPair ? 1u : 0u) | (p1 < kLimPair ? 4u : 0u)));
+    const float st = rho_max(crec[buf], ga0, nga) * rho_max(crec[buf] + kGa, gb0, ngb);
+    const uint32_t fl = __builtin_amdgcn_readfirstlane(st < kLimStage ? 7u : 0u);
     // the TM x TN tiles' chains run interleaved, block by block
     f32x16 p[TM][TN];
 #pragma unroll
