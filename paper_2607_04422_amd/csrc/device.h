@@ -115,6 +115,7 @@ struct BlockCand {
   uint32_t scale;   // E4M3 code
   uint64_t codes;   // 16 nibbles, element i in bits 4i..4i+3
   double err;       // sum of squared decode errors, element order, binary64
+  uint32_t k2;      // sum of (2 q)^2 over the block: twice-magnitudes squared
 };
 
 FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M) {
@@ -127,6 +128,7 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   const double half_ss = 0.5 * ((double)s * (double)sg);   // exact: 4 + 24 significant bits
   r.codes = 0;
   r.err = 0.0;
+  r.k2 = 0;
   if (rs > 0.0f) {
     const E2m1Thresholds th = e2m1_thresholds(rs);
 #pragma unroll
@@ -134,7 +136,9 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
       const uint32_t neg = __float_as_uint(u[i]) >> 31;
       const uint32_t idx = e2m1_index_thr(fabsf(u[i]), th);
       r.codes |= (uint64_t)((neg << 3) | idx) << (4 * i);
-      const double dec = (double)e2m1_twice(idx) * half_ss;   // exact q * s * s_g
+      const uint32_t tw = e2m1_twice(idx);
+      r.k2 += tw * tw;
+      const double dec = (double)tw * half_ss;   // exact q * s * s_g
       const double d = (double)u[i] - (neg ? -dec : dec);
       r.err = r.err + d * d;
     }
@@ -150,9 +154,13 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   return r;
 }
 
-// Quantise one (already rotated) block given the tensor scale.
+// Quantise one (already rotated) block given the tensor scale.  `n2` receives
+// sum_i (2 q_i)^2 M^2 with M the scale's integer significand (8..15, or the
+// mantissa of a subnormal scale): the block's sum of squared decoded values is
+// n2 2^(2 e - 22), e = max(exponent field, 1).
 FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_t& scale,
-                          uint64_t& codes) {
+                          uint64_t& codes, uint32_t& n2) {
+  n2 = 0;
   if (sg == 0.0f) {   // all-zero tensor: zero scales, zero magnitudes, signs kept
     codes = 0;
 #pragma unroll
@@ -170,6 +178,47 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
   }
   scale = c6.scale;
   codes = c6.codes;
+  const uint32_t mant = (scale >> 3) ? 8u + (scale & 7u) : (scale & 7u);
+  n2 = c6.k2 * mant * mant;
+}
+
+// Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a
+// stage in binary32 when rho sigma < 2^44, see gemm_fp4.hip):
+//   rho = max_b n2_b 4^(e_b - e_min),  e = max(exponent field, 1) over blocks with
+// a non-zero scale (a zero block adds nothing and does not lower e_min).
+FP4R_DEV uint32_t block_exp(uint32_t scale) {
+  return (scale & 0x7Fu) ? max((scale >> 3) & 15u, 1u) : 15u;
+}
+FP4R_DEV float stage_rho(const uint32_t (&n2)[4], const uint32_t (&e)[4]) {
+  const uint32_t emin = min(min(e[0], e[1]), min(e[2], e[3]));
+  float r = 0.0f;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) r = fmaxf(r, ldexpf((float)n2[b], 2 * (int)(e[b] - emin)));
+  return r;   // exact: n2 < 2^19 and the powers of two
+}
+
+// The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3.
+FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e) {
+  uint32_t qn[4], qe[4];
+  const int base = (int)(threadIdx.x & 60u);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    qn[k] = (uint32_t)__shfl((int)n2, base + k, 64);
+    qe[k] = (uint32_t)__shfl((int)e, base + k, 64);
+  }
+  return stage_rho(qn, qe);
+}
+
+// Maximum of non-negative values over the wave / over each 16 lanes.
+FP4R_DEV float wave_max_pos(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+FP4R_DEV float row16_max_pos(float v) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
 }
 
 // Global scale from the bit pattern of the (non-negative) amax.

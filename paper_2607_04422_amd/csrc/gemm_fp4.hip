@@ -25,8 +25,7 @@
 // sigma_j alike) the bound is below 2^24 u whenever |G|^2 rho_i sigma_j < 2^48;
 // then every partial sum is exactly representable in binary32, and the MFMAs
 // of the group may accumulate into one binary32 register, folded into binary64
-// once.  The loader computes rho per row for the whole 4-block stage, the
-// maximum over its 16 rows goes to LDS, and each
+// once.  The encoder stores rho per stage and 16 rows, and each
 // compute wave tests the maxima over its own rows (diagonal tiles of symmetric
 // products test tile-wide maxima, so that (i, j) and (j, i) add the same
 // binary32 values in the same order and the product stays exactly symmetric).
@@ -156,55 +155,24 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
   return q * s2;
 }
 
-// Chain bound of one stage (see the header).  `t` is the thread's block sum of
-// squares; lanes 4r + {0, 1, 2, 3} hold the four blocks of row r.  Writes max
-// rho over the loader wave's 16 rows (binary32 bit pattern; non-negative values
-// order as unsigned integers) to *rec.
-template <int CTRL>
-FP4R_DEV uint32_t dpp(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
-}
-constexpr int kDppSwap1 = 0xB1;     // quad_perm [1, 0, 3, 2]
-constexpr int kDppSwap2 = 0x4E;     // quad_perm [2, 3, 0, 1]
-constexpr int kDppRowRor4 = 0x124;  // rotate right by 4 within 16 lanes
-constexpr int kDppRowRor8 = 0x128;
-constexpr int kDppRowBcast15 = 0x142;   // lane 15 of each row to the next row
-constexpr int kDppRowBcast31 = 0x143;   // lane 31 to rows 2 and 3
+// Chain records of one operand: the encoder stores, per 64-element stage and 16
+// rows, the largest rho (see the header), [K/64][rows/16].  They are read through
+// the constant address space (written by an earlier kernel, never by this one),
+// so the wave-uniform loads below become scalar loads.
+typedef const float __attribute__((address_space(4))) cfloat;
 
-// Largest value over the wave, in lane 63 (non-negative binary32 bit patterns;
-// lanes a broadcast does not write read 0, which leaves the maximum alone).
-FP4R_DEV uint32_t wave_max_to_lane63(uint32_t v) {
-  v = max(v, dpp<kDppRowRor4>(v));
-  v = max(v, dpp<kDppRowRor8>(v));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppRowBcast15, 0xA, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppRowBcast31, 0xC, 0xF, false));
-  return v;
+// Largest record of groups [g0, g0 + n) of stage s, clamped to the operand's
+// groups (a tail tile's missing rows are zero and need no record).
+FP4R_DEV float rho_records_max(const float* rec, int64_t ngroups, int s, int g0, int n) {
+  cfloat* p = (cfloat*)(rec + (int64_t)s * ngroups);
+  float m = 0.0f;
+  for (int g = 0; g < n; ++g) m = fmaxf(m, p[min((int64_t)(g0 + g), ngroups - 1)]);
+  return m;
 }
 
-FP4R_DEV void fp4_chain_info(uint32_t scale, float t, uint32_t* rec) {
-  const uint32_t sc = scale & 0x7Fu;
-  // a zero block adds nothing to any group and leaves the row's minimum alone
-  const uint32_t e = sc ? max(sc >> 3, 1u) : 15u;
-  const uint32_t e2 = min(e, dpp<kDppSwap1>(e));
-  const uint32_t t2 = max(__float_as_uint(t), dpp<kDppSwap1>(__float_as_uint(t)));
-  const uint32_t e4 = min(e2, dpp<kDppSwap2>(e2));
-  const uint32_t t4 = max(t2, dpp<kDppSwap2>(t2));
-  const uint32_t r4 = wave_max_to_lane63(__float_as_uint(ldexpf(__uint_as_float(t4), 22 - 2 * (int)e4)));
-  if ((threadIdx.x & 63) == 63) *rec = r4;
-}
-
-// Largest of n records from g0 (wave-uniform), as binary32.
-FP4R_DEV float rho_max(const uint32_t* rec, int g0, int n) {
-  uint32_t m = 0;
-  for (int g = 0; g < n; ++g) m = max(m, rec[g0 + g]);
-  return __uint_as_float(m);
-}
-
-// Decodes the staged blocks into the LDS stage at `lds`; returns the (exact) sum
-// of squares of the thread's 16 decoded values.
+// Decodes the staged blocks into the LDS stage at `lds`.
 template <int ROWS, int NT>
-FP4R_DEV float fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
-  float t = 0.0f;
+FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
 #pragma unroll
   for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
     const int idx = threadIdx.x + NT * j;
@@ -221,16 +189,8 @@ FP4R_DEV float fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
       const int kbo = 32 * ROWS * kb + 64 * kb + 16 * (kb >> 1);   // lds_kb_base<ROWS>(kb)
       *reinterpret_cast<f16x8*>(lds + kbo + lds_row_off(r, half)) = v;
-#if FP4R_FP4_CHAIN
-      // squares of values with at most 6 significant bits: every partial sum is exact
-      t = __builtin_amdgcn_fdot2(p0, p0, t, false);
-      t = __builtin_amdgcn_fdot2(p1, p1, t, false);
-      t = __builtin_amdgcn_fdot2(p2, p2, t, false);
-      t = __builtin_amdgcn_fdot2(p3, p3, t, false);
-#endif
     }
   }
-  return t;
 }
 
 // ---------------------------------------------------------------------------
@@ -252,13 +212,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   constexpr int kStA = lds_stage_bytes<BM>(), kStB = lds_stage_bytes<BN>();
   constexpr size_t kMainBytes = (size_t)2 * (kStA + kStB);
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
-  constexpr int kGa = BM / 16, kGb = BN / 16;   // loader groups (16 rows) per operand tile
-  // chain records per buffer: [A loader groups][B loader groups]
-  constexpr int kRec = kGa + kGb;
-  constexpr size_t kRecBytes = FP4R_FP4_CHAIN ? (size_t)2 * kRec * sizeof(uint32_t) : 0;
-  constexpr size_t kLoopBytes = kMainBytes + kRecBytes;
-  __shared__ __attribute__((aligned(16))) char smem[kLoopBytes > kEpiBytes ? kLoopBytes : kEpiBytes];
-  uint32_t(*crec)[kRec] = reinterpret_cast<uint32_t(*)[kRec]>(smem + kMainBytes);
+  constexpr int kGa = BM / 16, kGb = BN / 16;   // 16-row groups per operand tile
+  __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
   char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
   char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
   constexpr bool kSym = MODE != kModeUpdateX;
@@ -287,8 +242,16 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   // diagonal tiles of symmetric products use all groups (see the header)
   const int uwave = __builtin_amdgcn_readfirstlane(wave);
   const bool diag = kSym && tm == tn;
-  const int ga0 = diag ? 0 : (uwave / WN_) * TM * 2, nga = diag ? kGa : TM * 2;
-  const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
+  const bool chain_on = g.a.rhog != nullptr && g.b.rhog != nullptr;
+  const int ga0 = (int)(row0 / 16) + (diag ? 0 : (uwave / WN_) * TM * 2), nga = diag ? kGa : TM * 2;
+  const int gb0 = (int)(col0 / 16) + (diag ? 0 : (uwave % WN_) * TN * 2), ngb = diag ? kGb : TN * 2;
+  const float* rec_a = chain_on ? g.a.rhog + mat * g.a.rhog_bstride : nullptr;
+  const float* rec_b = chain_on ? g.b.rhog + mat * g.b.rhog_bstride : nullptr;
+  // rho sigma of stage s for this wave's rows (+inf: do not chain)
+  auto stage_bound = [&](int s) {
+    if (!chain_on || s >= nstages) return __builtin_inff();
+    return rho_records_max(rec_a, g.M / 16, s, ga0, nga) * rho_records_max(rec_b, g.N / 16, s, gb0, ngb);
+  };
   // a stage chains as one group if 16 rho sigma < 2^48; the limit leaves room
   // for the rounding of the binary32 product rho * sigma
   constexpr float kLimStage = 17592186044416.0f * (1.0f - 1.0f / 65536.0f);   // 2^44 (1 - 2^-16)
@@ -296,28 +259,20 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 
   // stage -> LDS buffer `buf` (decoded operands and chain records)
   auto put = [&](int buf, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) {
-    const float ta = fp4_store<BM, NT>(lds_a[buf], xa);
-    const float tb = fp4_store<BN, NT>(lds_b[buf], xb);
-#if FP4R_FP4_CHAIN
-    fp4_chain_info(xa.scales[0], ta, crec[buf] + wave);
-    fp4_chain_info(xb.scales[0], tb, crec[buf] + kGa + wave);
-#else
-    (void)ta;
-    (void)tb;
-#endif
+    fp4_store<BM, NT>(lds_a[buf], xa);
+    fp4_store<BN, NT>(lds_b[buf], xb);
   };
 
   const f32x16 zero = {};
   // MFMAs and binary64 folds of the stage in LDS buffer `buf` (kbs blocks)
-  auto compute = [&](int buf, int kbs) {
+  auto compute = [&](int buf, int kbs, float st) {
     if (kbs <= 0) return;
     const char* la = lds_a[buf];
     const char* lb = lds_b[buf];
 #if FP4R_FP4_CHAIN
     // chain flags: bit k - 1 set = block k accumulates onto block k - 1 (blocks
     // past the end of K are zero in LDS and join any group)
-    const float st = rho_max(crec[buf], ga0, nga) * rho_max(crec[buf] + kGa, gb0, ngb);
-    const uint32_t fl = __builtin_amdgcn_readfirstlane(st < kLimStage ? 7u : 0u);
+    const uint32_t fl = st < kLimStage ? 7u : 0u;
     // the TM x TN tiles' chains run interleaved, block by block
     f32x16 p[TM][TN];
 #pragma unroll
@@ -388,14 +343,16 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   fp4_load<BM, NT>(src_a, nkb, 1, sa);
   fp4_load<BN, NT>(src_b, nkb, 1, sb);
   __syncthreads();
+  float st = stage_bound(0);
   auto step = [&](int s, int buf, Fp4Stage<BM, NT>& ha, Fp4Stage<BN, NT>& hb, Fp4Stage<BM, NT>& la2,
                   Fp4Stage<BN, NT>& lb2) {
     // unconditional: past the last stage every offset is out of range and reads 0,
     // and a branch here would make the waits below cover these loads too
     fp4_load<BM, NT>(src_a, nkb, s + 2, la2);
     fp4_load<BN, NT>(src_b, nkb, s + 2, lb2);
-    compute(buf, blocks_in(s));
+    compute(buf, blocks_in(s), st);
     put(buf ^ 1, ha, hb);
+    st = stage_bound(s + 1);
     __syncthreads();
   };
   // no data-dependent branch in the loop body (a stage past the end computes
@@ -405,12 +362,14 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     step(s + 1, 1, na, nb, sa, sb);
   }
 #else
+  float st = stage_bound(0);
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
     fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
     fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-    compute(s & 1, blocks_in(s));
+    compute(s & 1, blocks_in(s), st);
     put((s & 1) ^ 1, sa, sb);
+    st = stage_bound(s + 1);
     __syncthreads();
   }
   (void)na;

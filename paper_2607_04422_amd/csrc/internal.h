@@ -86,6 +86,10 @@ struct QOut {
   uint8_t* codes;
   uint8_t* scales;
   int64_t codes_bstride, scales_bstride;
+  // optional (axis 1 only, K = cols a multiple of 64): chain bound records, the
+  // largest rho over each 16 rows per 64-element stage, [K/64][rows/16]
+  float* rhog = nullptr;
+  int64_t rhog_bstride = 0;
 };
 
 // amax over rotated 16-blocks along `axis`; atomically maxes into
@@ -114,6 +118,8 @@ struct Fp4Operand {
   const uint8_t* codes;   // [rows][K/2]
   const uint8_t* scales;  // [rows][K/16]
   int64_t codes_bstride, scales_bstride;
+  const float* rhog = nullptr;  // [K/64][rows/16] chain bound records; null: no chaining
+  int64_t rhog_bstride = 0;
 };
 
 struct GemmFp4Args {

@@ -420,10 +420,20 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
     sc[b].sg[slot] = sg;
     if (tensor_scale) tensor_scale[b] = sg;
   }
-  if (g >= nblk) return;
+  // With chain records (axis 1, cols a multiple of 64) each wave takes 16 rows x
+  // one 64-column stage: lane 4i + k holds block k of row i, so the stage bound
+  // of a row and the record over the 16 rows reduce within the wave.
+  const bool want_rho = AXIS == 1 && out.rhog != nullptr;
+  if (g >= nblk) return;   // nblk is a multiple of 64 when records are requested
+  int64_t gb = g;
+  if (want_rho) {
+    const int64_t nst = in.cols / 64, wv = g >> 6;
+    const int lane = (int)(g & 63);
+    gb = ((wv / nst) * 16 + (lane >> 2)) * (in.cols / 16) + (wv % nst) * 4 + (lane & 3);
+  }
   float u[16];
   int64_t r, c;
-  load_block<AXIS>(in, b, g, u, r, c);
+  load_block<AXIS>(in, b, gb, u, r, c);
   if (clip) {
     const float tau = sc[b].tau;
 #pragma unroll
@@ -432,7 +442,13 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   if (rotate) rotate16(u, mask);
   uint32_t scale;
   uint64_t codes;
-  quant_block(u, sg, adaptive != 0, scale, codes);
+  uint32_t n2;
+  quant_block(u, sg, adaptive != 0, scale, codes, n2);
+  if (want_rho) {
+    const float rho = wave_max_pos(quad_stage_rho(n2, block_exp(scale)));
+    if ((threadIdx.x & 63) == 0)
+      out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
+  }
   int64_t code_off, scale_off;
   if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
     code_off = r * (in.cols / 2) + c / 2;
@@ -479,6 +495,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
   {
     const int i = threadIdx.x >> 2, q = threadIdx.x & 3;
     const int64_t r = r0 + i, c = c0 + 16 * q;
+    uint32_t n2 = 0, e = 15;
     if (r < m && c < n) {
       float u[16];
 #pragma unroll
@@ -486,15 +503,24 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       if (rotate) rotate16(u, mask);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgn, adaptive != 0, scale, codes);
+      quant_block(u, sgn, adaptive != 0, scale, codes, n2);
+      e = block_exp(scale);
       *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + r * (n / 2) + c / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
       qx.scales[b * qx.scales_bstride + r * (n / 16) + c / 16] = (uint8_t)scale;
+    }
+    // chain record of this wave's 16 rows for the tile's 64-column stage: lanes
+    // 4i .. 4i + 3 hold row i's four blocks (blocks past the edge count as zero)
+    if (qx.rhog) {
+      const float rho = wave_max_pos(quad_stage_rho(n2, e));
+      if ((threadIdx.x & 63) == 0 && r0 + 16 * (threadIdx.x >> 6) < m)
+        qx.rhog[b * qx.rhog_bstride + (c0 / 64) * (m / 16) + (r0 / 16) + (threadIdx.x >> 6)] = rho;
     }
   }
   {
     const int j = threadIdx.x & 63, q = threadIdx.x >> 6;   // column j, 16 rows at 16 q
     const int64_t c = c0 + j, r = r0 + 16 * q;
+    uint32_t n2 = 0, e = 15;
     if (r < m && c < n) {
       float u[16];
 #pragma unroll
@@ -502,10 +528,32 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       if (rotate) rotate16(u, mask);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgm, adaptive != 0, scale, codes);
+      quant_block(u, sgm, adaptive != 0, scale, codes, n2);
+      e = block_exp(scale);
       *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + c * (m / 2) + r / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
       qxt.scales[b * qxt.scales_bstride + c * (m / 16) + r / 16] = (uint8_t)scale;
+    }
+    if (qxt.rhog) {
+      // the stage's four blocks of column j sit in the four waves: exchange in LDS
+      // (the tile is no longer read once every thread has passed the barrier),
+      // then wave 0 reduces each 16 columns (16 rows of qXt) to a record
+      __syncthreads();
+      uint32_t* xn = reinterpret_cast<uint32_t*>(&tile[0][0]);
+      xn[q * 64 + j] = n2;
+      xn[256 + q * 64 + j] = e;
+      __syncthreads();
+      if (q == 0) {
+        uint32_t qn[4], qe[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          qn[k] = xn[k * 64 + j];
+          qe[k] = xn[256 + k * 64 + j];
+        }
+        const float rho = row16_max_pos(stage_rho(qn, qe));
+        if ((j & 15) == 0 && c < n)
+          qxt.rhog[b * qxt.rhog_bstride + (r0 / 64) * (n / 16) + c / 16] = rho;
+      }
     }
   }
 }
