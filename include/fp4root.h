@@ -56,7 +56,7 @@ extern "C" {
 enum {
   FP4ROOT_OK = 0,
   FP4ROOT_ERR_INVALID_ARG = -1, /* null pointer, bad count, bad flag or parameter */
-  FP4ROOT_ERR_SHAPE = -2,       /* a dimension is not a positive multiple of 16 or exceeds 2^21, or strides too small */
+  FP4ROOT_ERR_SHAPE = -2,       /* a dimension is not a positive multiple of 16 or exceeds 2^21, more than 2^36 elements, or strides too small */
   FP4ROOT_ERR_WORKSPACE = -3,   /* workspace null or smaller than the size query returned */
   FP4ROOT_ERR_NONFINITE = -4,   /* (device status) a NaN or Inf was met in an input */
   FP4ROOT_ERR_HIP = -5,         /* a HIP runtime call failed */

@@ -472,13 +472,23 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
       for (int k = 0; k < 16; ++k) cmax = fmaxf(cmax, fabsf(u[k]));
     }
   }
-  if (do_rows) {
-    const float w = warp_max(rmax);
-    if (lane == 0) atomicMax(&g.sc[mat].amax[g.amax_row_slot], __float_as_uint(w));
-  }
-  if (do_cols) {
-    const float w = warp_max(cmax);
-    if (lane == 0) atomicMax(&g.sc[mat].amax[g.amax_col_slot], __float_as_uint(w));
+  // one maximum per direction and workgroup (the tile is no longer read after
+  // the barrier), recorded on the workgroup's amax line
+  if (do_rows || do_cols) {
+    const float wr = warp_max(rmax), wc = warp_max(cmax);
+    __syncthreads();
+    float* red = tile;
+    if (lane == 0) {
+      red[wave] = wr;
+      red[NT / 64 + wave] = wc;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2 && (threadIdx.x == 0 ? do_rows : do_cols)) {
+      float m = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NT / 64; ++w) m = fmaxf(m, red[threadIdx.x * (NT / 64) + w]);
+      amax_record(&g.sc[mat], threadIdx.x == 0 ? g.amax_row_slot : g.amax_col_slot, blockIdx.x, m);
+    }
   }
 }
 

@@ -30,14 +30,35 @@ struct MatChunk {
 };
 
 // Per-matrix scalars kept in the workspace (one struct per matrix).
+// Amax records are maxima over many workgroups.  To keep same-address atomics
+// few, each slot is spread over kAmaxSpread 64-byte lines (a workgroup adds its
+// maximum to line (workgroup index mod kAmaxSpread)); readers take the maximum
+// of the lines.
+constexpr int kAmaxSpread = 8;
+struct alignas(64) AmaxLine {
+  uint32_t v[16];        // slot k in v[k] (bit patterns of non-negative binary32)
+};
+
 struct MatScalars {
-  uint32_t amax[6];      // bit patterns: X along n / along m (two pairs, alternating by step), A, B
+  AmaxLine amax[kAmaxSpread];   // slots: X along n / along m (two pairs, alternating by step), A, B
   float sg[6];           // tensor scales derived from amax
   float tau;             // clip threshold (+inf without clipping)
   float inv_norm;        // 1 / (||X'||_F + eps)
   uint32_t sel_prefix[2];  // radix select state for ranks lo and lo + 1
   uint32_t sel_rank[2];
 };
+
+// Record a non-negative maximum in amax slot `slot` (line chosen by `spread`),
+// and read a slot back.
+__device__ inline void amax_record(MatScalars* s, int slot, uint32_t spread, float v) {
+  atomicMax(&s->amax[spread % kAmaxSpread].v[slot], __float_as_uint(v));
+}
+__device__ inline uint32_t amax_read(const MatScalars& s, int slot) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < kAmaxSpread; ++i) m = m > s.amax[i].v[slot] ? m : s.amax[i].v[slot];
+  return m;
+}
 
 // amax / tensor-scale slots.  The X slots alternate between steps so that the
 // update product of step k can record the amaxes of X_{k+1} while step k still
@@ -93,11 +114,11 @@ struct QOut {
 };
 
 // amax over rotated 16-blocks along `axis`; atomically maxes into
-// sc[b].amax[slot].  tau: clamp each element to +-sc[b].tau first when clip != 0.
+// amax slot `slot` of sc[b].  tau: clamp each element to +-sc[b].tau first when clip != 0.
 hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                        MatScalars* sc, int slot, uint32_t* status, hipStream_t st);
 
-// Encode with the tensor scale derived from sc[b].amax[slot]; writes sc[b].sg[slot]
+// Encode with the tensor scale derived from amax slot `slot` of sc[b]; writes sc[b].sg[slot]
 // and, when tensor_scale != nullptr, tensor_scale[b].
 hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,

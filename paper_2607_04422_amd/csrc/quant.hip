@@ -297,8 +297,8 @@ __global__ __launch_bounds__(256) void k_prep_copy(MatChunk ch, MatScalars* sc, 
   __syncthreads();
   const float bc = block_max_256(mc, red);
   if (threadIdx.x == 0) {
-    atomicMax(&sc[mi].amax[slot_n], __float_as_uint(br));
-    atomicMax(&sc[mi].amax[slot_m], __float_as_uint(bc));
+    amax_record(&sc[mi], slot_n, blockIdx.x, br);
+    amax_record(&sc[mi], slot_m, blockIdx.x, bc);
   }
 }
 
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(256) void k_amax(Batch in, uint32_t mask, int rotat
   __syncthreads();
   if (threadIdx.x == 0) {
     const float mm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    atomicMax(&sc[b].amax[slot], __float_as_uint(mm));
+    amax_record(&sc[b], slot, blockIdx.x, mm);
   }
 }
 
@@ -415,7 +415,7 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   const int64_t b = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t nblk = in.rows * in.cols / 16;
-  const float sg = tensor_scale_from_amax(sc[b].amax[slot]);
+  const float sg = tensor_scale_from_amax(amax_read(sc[b], slot));
   if (g == 0) {
     sc[b].sg[slot] = sg;
     if (tensor_scale) tensor_scale[b] = sg;
@@ -473,8 +473,8 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
   const int64_t tn = cdiv(n, kT);
   const int64_t r0 = (blockIdx.x / tn) * kT, c0 = (blockIdx.x % tn) * kT;
   const float* X = x + b * x_bstride;
-  const float sgn = tensor_scale_from_amax(sc[b].amax[slot_n]);
-  const float sgm = tensor_scale_from_amax(sc[b].amax[slot_m]);
+  const float sgn = tensor_scale_from_amax(amax_read(sc[b], slot_n));
+  const float sgm = tensor_scale_from_amax(amax_read(sc[b], slot_m));
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     sc[b].sg[slot_n] = sgn;
     sc[b].sg[slot_m] = sgm;
@@ -644,7 +644,9 @@ __global__ void k_reset_scalars(MatScalars* sc, int64_t n, uint32_t slot_mask, i
   MatScalars& s = sc[i];
 #pragma unroll
   for (int k = 0; k < kNumSlots; ++k)
-    if ((slot_mask >> k) & 1u) s.amax[k] = 0u;
+    if ((slot_mask >> k) & 1u)
+#pragma unroll
+      for (int l = 0; l < kAmaxSpread; ++l) s.amax[l].v[k] = 0u;
   if (full) {
 #pragma unroll
     for (int k = 0; k < kNumSlots; ++k) s.sg[k] = 0.0f;
