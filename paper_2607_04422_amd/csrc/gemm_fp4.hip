@@ -156,9 +156,15 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
 }
 
 // Chain records of one operand: the encoder stores, per 64-element stage and 16
-// rows, the largest rho (see the header), [K/64][rows/16].  They are read through
-// the constant address space (written by an earlier kernel, never by this one),
-// so the wave-uniform loads below become scalar loads.
+// rows, the largest rho (see the header), [K/64][rows/16].  Two ways to bring
+// them to a compute wave (chosen per product by measurement):
+// * table: before the stage loop each wave evaluates rho sigma over its own row
+//   groups for every stage (one stage per lane) into its column of an LDS table,
+//   so the loop reads one value per stage (K up to 64 kRecStages);
+// * scalar: per stage the wave reads its groups' records through the constant
+//   address space (written by an earlier kernel, never by this one), so the
+//   wave-uniform loads become scalar loads, one stage ahead.
+constexpr int kRecStages = 256;   // table: longer K (over 16384) folds every block
 typedef const float __attribute__((address_space(4))) cfloat;
 
 // Largest record of groups [g0, g0 + n) of stage s, clamped to the operand's
@@ -214,6 +220,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
   constexpr int kGa = BM / 16, kGb = BN / 16;   // 16-row groups per operand tile
   __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
+  constexpr bool kTable = MODE != kModeUpdateX;   // record delivery (see above)
+  __shared__ float wbound[FP4R_FP4_CHAIN && kTable ? kRecStages : 1][NT / 64];
   char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
   char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
   constexpr bool kSym = MODE != kModeUpdateX;
@@ -242,22 +250,50 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   // diagonal tiles of symmetric products use all groups (see the header)
   const int uwave = __builtin_amdgcn_readfirstlane(wave);
   const bool diag = kSym && tm == tn;
-  const bool chain_on = g.a.rhog != nullptr && g.b.rhog != nullptr;
-  const int ga0 = (int)(row0 / 16) + (diag ? 0 : (uwave / WN_) * TM * 2), nga = diag ? kGa : TM * 2;
-  const int gb0 = (int)(col0 / 16) + (diag ? 0 : (uwave % WN_) * TN * 2), ngb = diag ? kGb : TN * 2;
+  const bool chain_on = g.a.rhog != nullptr && g.b.rhog != nullptr && (!kTable || nstages <= kRecStages);
+  const int ga0 = diag ? 0 : (uwave / WN_) * TM * 2, nga = diag ? kGa : TM * 2;
+  const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
   const float* rec_a = chain_on ? g.a.rhog + mat * g.a.rhog_bstride : nullptr;
   const float* rec_b = chain_on ? g.b.rhog + mat * g.b.rhog_bstride : nullptr;
-  // rho sigma of stage s for this wave's rows (+inf: do not chain)
+  // rho sigma of stages s0 .. s0 + kRecStages - 1 for this wave's rows into
+  // wbound[.][wave] (+inf without records or past the last stage; missing groups
+  // of a tail tile read 0: their rows are zero).  Only this wave touches its
+  // column, so no barrier is needed.
+  auto fill_bounds = [&](int s0) {
+    if (!kTable) return;
+    const int64_t nga_all = g.M / 16, ngb_all = g.N / 16;
+#pragma unroll
+    for (int h = 0; h < kRecStages / 64; ++h) {
+      const int ss = lane + 64 * h;
+      const int64_t sg = (int64_t)s0 + ss;
+      float v = __builtin_inff();
+      if (chain_on && sg < nstages) {
+        float ma = 0.0f, mb = 0.0f;
+        for (int k = 0; k < nga; ++k) {
+          const int64_t grp = row0 / 16 + ga0 + k;
+          if (grp < nga_all) ma = fmaxf(ma, rec_a[sg * nga_all + grp]);
+        }
+        for (int k = 0; k < ngb; ++k) {
+          const int64_t grp = col0 / 16 + gb0 + k;
+          if (grp < ngb_all) mb = fmaxf(mb, rec_b[sg * ngb_all + grp]);
+        }
+        v = ma * mb;
+      }
+      wbound[ss][wave] = v;
+    }
+  };
   auto stage_bound = [&](int s) {
+    if (kTable) return wbound[s % kRecStages][wave];
     if (!chain_on || s >= nstages) return __builtin_inff();
-    return rho_records_max(rec_a, g.M / 16, s, ga0, nga) * rho_records_max(rec_b, g.N / 16, s, gb0, ngb);
+    return rho_records_max(rec_a, g.M / 16, s, (int)(row0 / 16) + ga0, nga) *
+           rho_records_max(rec_b, g.N / 16, s, (int)(col0 / 16) + gb0, ngb);
   };
   // a stage chains as one group if 16 rho sigma < 2^48; the limit leaves room
   // for the rounding of the binary32 product rho * sigma
   constexpr float kLimStage = 17592186044416.0f * (1.0f - 1.0f / 65536.0f);   // 2^44 (1 - 2^-16)
 #endif
 
-  // stage -> LDS buffer `buf` (decoded operands and chain records)
+  // stage -> LDS buffer `buf` (decoded operands)
   auto put = [&](int buf, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) {
     fp4_store<BM, NT>(lds_a[buf], xa);
     fp4_store<BN, NT>(lds_b[buf], xb);
@@ -336,6 +372,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   fp4_load<BM, NT>(src_a, nkb, 0, sa);
   fp4_load<BN, NT>(src_b, nkb, 0, sb);
   put(0, sa, sb);
+  if (FP4R_FP4_CHAIN) fill_bounds(0);
 #if FP4R_FP4_PREFETCH == 2
   // Stage s is computed from LDS while stage s + 1 waits in one register set and
   // stage s + 2 loads into the other; the loop body runs two stages with the
@@ -343,16 +380,16 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   fp4_load<BM, NT>(src_a, nkb, 1, sa);
   fp4_load<BN, NT>(src_b, nkb, 1, sb);
   __syncthreads();
-  float st = stage_bound(0);
+  float st = kTable ? 0.0f : stage_bound(0);
   auto step = [&](int s, int buf, Fp4Stage<BM, NT>& ha, Fp4Stage<BN, NT>& hb, Fp4Stage<BM, NT>& la2,
                   Fp4Stage<BN, NT>& lb2) {
     // unconditional: past the last stage every offset is out of range and reads 0,
     // and a branch here would make the waits below cover these loads too
     fp4_load<BM, NT>(src_a, nkb, s + 2, la2);
     fp4_load<BN, NT>(src_b, nkb, s + 2, lb2);
-    compute(buf, blocks_in(s), st);
+    compute(buf, blocks_in(s), kTable ? stage_bound(s) : st);
     put(buf ^ 1, ha, hb);
-    st = stage_bound(s + 1);
+    if (!kTable) st = stage_bound(s + 1);
     __syncthreads();
   };
   // no data-dependent branch in the loop body (a stage past the end computes
@@ -362,14 +399,14 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     step(s + 1, 1, na, nb, sa, sb);
   }
 #else
-  float st = stage_bound(0);
+  float st = kTable ? 0.0f : stage_bound(0);
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
     fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
     fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-    compute(s & 1, blocks_in(s), st);
+    compute(s & 1, blocks_in(s), kTable ? stage_bound(s) : st);
     put((s & 1) ^ 1, sa, sb);
-    st = stage_bound(s + 1);
+    if (!kTable) st = stage_bound(s + 1);
     __syncthreads();
   }
   (void)na;
