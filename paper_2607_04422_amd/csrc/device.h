@@ -24,8 +24,7 @@ constexpr float kSgDivisor = 2688.0f;
 // H diag(d) y / 4, the transpose of the same map.  (Sections 2, 3.4.)
 FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
-    if ((mask >> i) & 1u) u[i] = -u[i];
+  for (int i = 0; i < 16; ++i) u[i] = __uint_as_float(__float_as_uint(u[i]) ^ (((mask >> i) & 1u) << 31));
 #pragma unroll
   for (int h = 1; h < 16; h <<= 1) {
 #pragma unroll
@@ -105,17 +104,17 @@ FP4R_DEV uint32_t e2m1_index_thr(float a, const E2m1Thresholds& th) {
          (uint32_t)(a > th.t[6]);
 }
 
-// Twice the E2M1 magnitude of an index: {0, 1, 2, 3, 4, 6, 8, 12}.
-FP4R_DEV uint32_t e2m1_twice(uint32_t idx) {
-  return idx < 4 ? idx : ((2u + (idx & 1u)) << ((idx >> 1) - 1u));
-}
+// Twice the E2M1 magnitude of an index: {0, 1, 2, 3, 4, 6, 8, 12} (one nibble each).
+FP4R_DEV uint32_t e2m1_twice(uint32_t idx) { return (0xC8643210u >> (idx << 2)) & 15u; }
 
 // One candidate block scaling (block maximum mapped to M * s * s_g).
 struct BlockCand {
   uint32_t scale;   // E4M3 code
   uint64_t codes;   // 16 nibbles, element i in bits 4i..4i+3
-  double err;       // sum of squared decode errors, element order, binary64
   uint32_t k2;      // sum of (2 q)^2 over the block: twice-magnitudes squared
+  float err;        // sum of squared decode errors in binary32 (fma, element order)
+  float s2;         // (s s_g)^2 in binary32, for the error bound
+  double half_ss;   // 0.5 s s_g, exact
 };
 
 FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M) {
@@ -125,39 +124,61 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   r.scale = e4m3_rne(v);
   const float s = e4m3_value(r.scale);
   const float rs = s * sg;
-  const double half_ss = 0.5 * ((double)s * (double)sg);   // exact: 4 + 24 significant bits
+  r.half_ss = 0.5 * ((double)s * (double)sg);   // exact: 4 + 24 significant bits
+  r.s2 = rs * rs;
   r.codes = 0;
-  r.err = 0.0;
+  r.err = 0.0f;
   r.k2 = 0;
   if (rs > 0.0f) {
     const E2m1Thresholds th = e2m1_thresholds(rs);
+    const float h = 0.5f * rs;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const uint32_t neg = __float_as_uint(u[i]) >> 31;
-      const uint32_t idx = e2m1_index_thr(fabsf(u[i]), th);
+      const float a = fabsf(u[i]);
+      const uint32_t idx = e2m1_index_thr(a, th);
       r.codes |= (uint64_t)((neg << 3) | idx) << (4 * i);
       const uint32_t tw = e2m1_twice(idx);
       r.k2 += tw * tw;
-      const double dec = (double)tw * half_ss;   // exact q * s * s_g
-      const double d = (double)u[i] - (neg ? -dec : dec);
-      r.err = r.err + d * d;
+      const float d = fmaf(-(float)tw, h, a);
+      r.err = fmaf(d, d, r.err);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const uint32_t neg = __float_as_uint(u[i]) >> 31;
       r.codes |= (uint64_t)(neg << 3) << (4 * i);
-      const double d = (double)u[i];
-      r.err = r.err + d * d;
+      r.err = fmaf(u[i], u[i], r.err);
     }
   }
   return r;
+}
+
+// The candidate's squared error in binary64, summed in element order: the
+// reference definition of the 4/6 choice.
+FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c) {
+  double e = 0.0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const double dec = (double)e2m1_twice((uint32_t)(c.codes >> (4 * i)) & 7u) * c.half_ss;
+    const double d = (double)fabsf(u[i]) - dec;   // exact; d^2 as for the signed difference
+    e = e + d * d;
+  }
+  return e;
 }
 
 // Quantise one (already rotated) block given the tensor scale.  `n2` receives
 // sum_i (2 q_i)^2 M^2 with M the scale's integer significand (8..15, or the
 // mantissa of a subnormal scale): the block's sum of squared decoded values is
 // n2 2^(2 e - 22), e = max(exponent field, 1).
+//
+// Adaptive 4/6 keeps M = 4 iff its binary64 squared error is strictly smaller.
+// The binary32 sums decide when they are far apart: with S = s s_g, decoded
+// values |dec_i| <= 6 S and D_i the exact errors, each fma-computed difference
+// is within 2^-24 (|dec_i| + |D_i|) of D_i and the sum adds 16 roundings, so
+// |err32 - E| <= 2^-24 (E + 576 S^2) + 2^-19.8 E < 2^-14 S^2 + 2^-19 E =: B.
+// If err4 + 2 (B4 + B6) < err6 the exact E4 < E6 by more than any binary64
+// rounding, and symmetrically; otherwise both are recomputed in binary64.
 FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_t& scale,
                           uint64_t& codes, uint32_t& n2) {
   n2 = 0;
@@ -173,8 +194,13 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
   for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, fabsf(u[i]));
   BlockCand c6 = quant_candidate(u, bmax, sg, 6.0f);
   if (adaptive) {
-    BlockCand c4 = quant_candidate(u, bmax, sg, 4.0f);
-    if (c4.err < c6.err) c6 = c4;
+    const BlockCand c4 = quant_candidate(u, bmax, sg, 4.0f);
+    const float b = 2.0f * (0x1p-14f * (c4.s2 + c6.s2) + 0x1p-18f * (c4.err + c6.err));
+    bool use4;
+    if (c4.err + b < c6.err) use4 = true;
+    else if (c6.err + b < c4.err) use4 = false;
+    else use4 = cand_err64(u, c4) < cand_err64(u, c6);
+    if (use4) c6 = c4;
   }
   scale = c6.scale;
   codes = c6.codes;
