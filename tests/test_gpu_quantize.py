@@ -100,3 +100,35 @@ def test_quantize_full_size_sampled_rows():
         ref = quantize(m, axis, rht.step_signs(5, 1), True, rows=sel)
         got = gpu_nvfp4(codes[sel], scales[sel], sg)
         assert_same_nvfp4(got, ref, f"full-size axis={axis}")
+
+
+def test_quantize_adaptive_near_ties():
+    """Blocks whose two 4/6 candidates have equal or nearly equal squared errors
+    (a single spike representable under both scalings, spikes on the E4M3 grid,
+    two-level blocks), where the binary32 error sums cannot decide and the
+    binary64 recomputation must reproduce the reference choice (keep M = 4 only
+    if strictly smaller)."""
+    rng = np.random.default_rng(21)
+    rows, cols = 64, 256
+    m = np.zeros((rows, cols), np.float32)
+    m[0, 0] = 2688.0                                  # amax: s_g = 1
+    for r in range(rows):
+        for b in range(cols // 16):
+            blk = m[r, 16 * b:16 * b + 16]
+            kind = (r + b) % 4
+            e4 = 2.0 ** int(rng.integers(-6, 8))
+            if kind == 0:      # one spike: 6 s and 4 (1.5 s) both exact
+                blk[int(rng.integers(16))] = np.float32(6.0 * e4)
+            elif kind == 1:    # two levels on both grids
+                blk[:8] = np.float32(6.0 * e4)
+                blk[8:] = np.float32(3.0 * e4)
+            elif kind == 2:    # grid values plus a tiny perturbation
+                blk[:] = np.float32(6.0 * e4) * (1 + np.float32(2.0 ** -20) * rng.standard_normal(16).astype(np.float32))
+            else:              # random
+                blk[:] = rng.standard_normal(16).astype(np.float32) * np.float32(e4)
+    m[0, 0] = 2688.0
+    x = torch.from_numpy(m).cuda()
+    for axis in (1, 0):
+        codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=axis, flags=F.F_ADAPTIVE46, seed=0)
+        ref = quantize(m, axis, None, True)
+        assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"near ties axis={axis}")
