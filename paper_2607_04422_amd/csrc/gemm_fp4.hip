@@ -200,6 +200,97 @@ FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
 }
 
 // ---------------------------------------------------------------------------
+// Rotated amaxes of an output, for the tensor scale of the operand encoded from
+// it next (Section 3.2: the scale follows the largest magnitude after the 16-point
+// rotation).  The rotation is the encoder's binary32 butterfly (signs, strides 1,
+// 2, 4, 8, factor 1/4); only the largest magnitude is wanted, which permits three
+// exact shortcuts:
+// * the signs enter the stride-1 stage: fl(s_i u_i +- s_j u_j) is one fma of exact
+//   products;
+// * a stage across lanes may produce the difference with its sign flipped in the
+//   lane holding the higher position: the later stages pair positions that agree
+//   in that bit, so the flip reaches the final value unchanged (a sign only);
+// * of the last stage's pair fl(p + q), fl(p - q) the larger magnitude is
+//   fl(|p| + |q|), and the factor 1/4 commutes with the maximum (rounding is
+//   monotone), so it is applied once to the final maximum.
+
+template <int CTRL>
+FP4R_DEV float dpp_f(float v) {
+  // every source lane of the patterns used here exists (bound_ctrl only spares the old value)
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+// Row direction, four consecutive elements per lane: lane p = lane % 4 of a quad
+// holds positions 4p .. 4p + 3 of a 16-element block; sg = their signs (+-1),
+// s4 = +1 for even p, -1 for odd p.  Returns the unscaled maximum magnitude of
+// the quad's block (every lane of the quad gets the same value).  All lanes of
+// the wave must be active.
+FP4R_DEV float rot_rows_max4(float4 u, const float (&sg)[4], float s4) {
+  const float t1 = sg[1] * u.y, t3 = sg[3] * u.w;
+  const float a0 = __builtin_fmaf(sg[0], u.x, t1), a1 = __builtin_fmaf(sg[0], u.x, -t1);
+  const float a2 = __builtin_fmaf(sg[2], u.z, t3), a3 = __builtin_fmaf(sg[2], u.z, -t3);
+  const float b0 = a0 + a2, b2 = a0 - a2, b1 = a1 + a3, b3 = a1 - a3;
+  // stride 4: partner p ^ 1
+  const float c0 = __builtin_fmaf(dpp_f<kDppXor1>(b0), s4, b0);
+  const float c1 = __builtin_fmaf(dpp_f<kDppXor1>(b1), s4, b1);
+  const float c2 = __builtin_fmaf(dpp_f<kDppXor1>(b2), s4, b2);
+  const float c3 = __builtin_fmaf(dpp_f<kDppXor1>(b3), s4, b3);
+  // stride 8: partner p ^ 2
+  const float m0 = fabsf(c0) + fabsf(dpp_f<kDppXor2>(c0));
+  const float m1 = fabsf(c1) + fabsf(dpp_f<kDppXor2>(c1));
+  const float m2 = fabsf(c2) + fabsf(dpp_f<kDppXor2>(c2));
+  const float m3 = fabsf(c3) + fabsf(dpp_f<kDppXor2>(c3));
+  return fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
+}
+
+// Column direction, on the MFMA 32x32 output layout: v[B .. B + 7] of a lane are
+// rows (e & 3) + 4 hb + 8 (e >> 2), e = 0 .. 7, of a 16-row block of its column
+// (hb = lane / 32); sg = the signs of those rows, s4 = +1 (hb = 0) or -1.
+// Returns the unscaled maximum magnitude over the lane's 8 outputs.  All lanes of
+// the wave must be active.
+template <int B>
+FP4R_DEV float rot_cols_max8(const float (&v)[16], const float (&sg)[8], float s4) {
+  float a[8], b[8], c[8];
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    const float t = sg[e + 1] * v[B + e + 1];
+    a[e] = __builtin_fmaf(sg[e], v[B + e], t);
+    a[e + 1] = __builtin_fmaf(sg[e], v[B + e], -t);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; e += 4) {
+    b[e] = a[e] + a[e + 2];
+    b[e + 2] = a[e] - a[e + 2];
+    b[e + 1] = a[e + 1] + a[e + 3];
+    b[e + 3] = a[e + 1] - a[e + 3];
+  }
+  // stride 4: both halves' values of the pair in every lane
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const auto lh = __builtin_amdgcn_permlane32_swap(__float_as_uint(b[e]), __float_as_uint(b[e]), false, false);
+    c[e] = __builtin_fmaf(__uint_as_float(lh[1]), s4, __uint_as_float(lh[0]));
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(c[e]) + fabsf(c[e + 4]));
+  return m;
+}
+
+// Maximum of a non-negative value over the wave (bit pattern, uniform).
+FP4R_DEV uint32_t wave_max_bits(float v) {
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  const uint32_t b = __float_as_uint(v);
+  const uint32_t r0 = __builtin_amdgcn_readlane(b, 0), r1 = __builtin_amdgcn_readlane(b, 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(b, 32), r3 = __builtin_amdgcn_readlane(b, 48);
+  const uint32_t m01 = r0 > r1 ? r0 : r1, m23 = r2 > r3 ? r2 : r3;
+  return m01 > m23 ? m01 : m23;
+}
+
+// ---------------------------------------------------------------------------
 // Exact NVFP4 product.
 
 #ifndef FP4R_FP4_WAVES_PER_EU
@@ -214,7 +305,9 @@ template <int MODE, int WM_, int WN_, int TM, int TN>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) {
   constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
-  constexpr int kLdT = BN + 1;   // padded row of the FP32 output tile staged in LDS
+  // padded row of the FP32 output tile staged in LDS: rows stay 16-byte aligned, and
+  // the two half-waves of an MFMA-layout write (rows 4 apart) fall 32 banks apart
+  constexpr int kLdT = BN + 8;
   constexpr int kStA = lds_stage_bytes<BM>(), kStB = lds_stage_bytes<BN>();
   constexpr size_t kMainBytes = (size_t)2 * (kStA + kStB);
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
@@ -222,6 +315,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
   constexpr bool kTable = MODE != kModeUpdateX;   // record delivery (see above)
   __shared__ float wbound[FP4R_FP4_CHAIN && kTable ? kRecStages : 1][NT / 64];
+  __shared__ uint32_t red[2][NT / 64];   // per-wave amaxes (rows, columns)
   char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
   char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
   constexpr bool kSym = MODE != kModeUpdateX;
@@ -440,6 +534,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
           xin[i][j][e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)off, 0, 0));
         }
   }
+  // this lane's outputs in binary32 (zero outside the matrix), also staged in LDS
+  float val[TM][TN][16];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -452,79 +548,103 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
         if (MODE == kModeGramB) v = cb * (double)xin[i][j][e] + cc * v;
         if (MODE == kModeUpdateX) v = ca * (double)xin[i][j][e] + v;
         const bool in = row0 + rl < g.M && col0 + cl < g.N;
-        tile[rl * kLdT + cl] = in ? (float)v : 0.0f;
+        val[i][j][e] = in ? (float)v : 0.0f;
+        tile[rl * kLdT + cl] = val[i][j][e];
       }
-  __syncthreads();
-  // coalesced stores: rows of the tile, and (off-diagonal symmetric tiles) its transpose
+  // off-diagonal tiles of symmetric products: the transposed tile straight from
+  // registers (four consecutive rows of a column form a row segment of it)
   const bool mirror = kSym && tm != tn;
-  constexpr int kSegs = BN / 16;                 // 16-float segments per row
-  for (int idx = threadIdx.x; idx < BM * kSegs; idx += NT) {
-    const int rl = idx / kSegs, q = idx % kSegs;
-    const int64_t r = row0 + rl, c = col0 + 16 * q;
-    if (r < g.M && c < g.N) {
-      float4* dst = reinterpret_cast<float4*>(out + r * g.N + c);
+  if (mirror) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        dst[k] = make_float4(tile[rl * kLdT + 16 * q + 4 * k], tile[rl * kLdT + 16 * q + 4 * k + 1],
-                             tile[rl * kLdT + 16 * q + 4 * k + 2], tile[rl * kLdT + 16 * q + 4 * k + 3]);
-    }
-    if (mirror) {
-      // row cl of the mirrored tile = column cl of this tile
-      const int cl = rl;
-      const int64_t mr = col0 + cl, mc = row0 + 16 * q;
-      if (mr < g.N && mc < g.M) {
-        float4* dst = reinterpret_cast<float4*>(out + mr * g.N + mc);
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          dst[k] = make_float4(tile[(16 * q + 4 * k) * kLdT + cl], tile[(16 * q + 4 * k + 1) * kLdT + cl],
-                               tile[(16 * q + 4 * k + 2) * kLdT + cl], tile[(16 * q + 4 * k + 3) * kLdT + cl]);
-      }
-    }
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int rb = (wm * TM + i) * 32 + 8 * e4 + 4 * (lane >> 5);
+          const int cl = (wn * TN + j) * 32 + (lane & 31);
+          const int64_t mr = col0 + cl, mc = row0 + rb;
+          if (mr < g.N && mc < g.M)
+            *reinterpret_cast<float4*>(out + mr * g.N + mc) =
+                make_float4(val[i][j][4 * e4], val[i][j][4 * e4 + 1], val[i][j][4 * e4 + 2], val[i][j][4 * e4 + 3]);
+        }
   }
-  // rotated amaxes of the output: 16-column blocks of every row, and 16-row blocks
-  // of every column (the mirrored tile's rows, or X_{k+1} along m)
+  // rotated amaxes: 16-row blocks of every column (the mirrored tile's rows, or
+  // X_{k+1} along m) from registers, 16-column blocks of every row from LDS
   const bool do_rows = g.amax_row_slot >= 0;
   const bool do_cols = g.amax_col_slot >= 0 && (!kSym || mirror);
-  float rmax = 0.0f, cmax = 0.0f;
-  if (do_rows) {
-    for (int idx = threadIdx.x; idx < BM * kSegs; idx += NT) {
-      const int rl = idx / kSegs, q = idx % kSegs;
-      float u[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) u[k] = tile[rl * kLdT + 16 * q + k];
-      if (g.amax_rotate) rotate16(u, g.amax_mask);
-#pragma unroll
-      for (int k = 0; k < 16; ++k) rmax = fmaxf(rmax, fabsf(u[k]));
-    }
-  }
+  float cmax = 0.0f, rmax = 0.0f;
   if (do_cols) {
-    constexpr int kRsegs = BM / 16;
-    for (int idx = threadIdx.x; idx < BN * kRsegs; idx += NT) {
-      const int cl = idx % BN, q = idx / BN;
-      float u[16];
+    if (g.amax_rotate) {
+      const int hb = lane >> 5;
+      float sg[8];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) u[k] = tile[(16 * q + k) * kLdT + cl];
-      if (g.amax_rotate) rotate16(u, g.amax_mask);
+      for (int e = 0; e < 8; ++e)
+        sg[e] = ((g.amax_mask >> ((e & 3) + 4 * hb + 8 * (e >> 2))) & 1u) ? -1.0f : 1.0f;
+      const float s4 = hb ? -1.0f : 1.0f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) cmax = fmaxf(cmax, fabsf(u[k]));
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          cmax = fmaxf(cmax, rot_cols_max8<0>(val[i][j], sg, s4));
+          cmax = fmaxf(cmax, rot_cols_max8<8>(val[i][j], sg, s4));
+        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) cmax = fmaxf(cmax, fabsf(val[i][j][e]));
     }
   }
-  // one maximum per direction and workgroup (the tile is no longer read after
-  // the barrier), recorded on the workgroup's amax line
+  __syncthreads();
+  // rows of the tile: 32 lanes per row, one 16-byte slot each (coalesced stores;
+  // a quad of lanes holds one 16-column block)
+  {
+    constexpr int kSlots = BN / 4;
+    static_assert(NT % kSlots == 0 && (BM * kSlots) % NT == 0, "the row pass covers the tile");
+    const int p = lane & 3;
+    float sg[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) sg[w] = ((g.amax_mask >> (4 * p + w)) & 1u) ? -1.0f : 1.0f;
+    const float s4 = (p & 1) ? -1.0f : 1.0f;
+    constexpr int kIt = BM * kSlots / NT;
+    float4 u[kIt];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      const int idx = threadIdx.x + NT * it;
+      u[it] = *reinterpret_cast<const float4*>(tile + (idx / kSlots) * kLdT + 4 * (idx % kSlots));
+    }
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      const int idx = threadIdx.x + NT * it;
+      const int64_t r = row0 + idx / kSlots, c = col0 + 4 * (idx % kSlots);
+      if (r < g.M && c < g.N) *reinterpret_cast<float4*>(out + r * g.N + c) = u[it];
+    }
+    if (do_rows && g.amax_rotate) {
+#pragma unroll
+      for (int it = 0; it < kIt; ++it) rmax = fmaxf(rmax, rot_rows_max4(u[it], sg, s4));
+    } else if (do_rows) {
+#pragma unroll
+      for (int it = 0; it < kIt; ++it)
+        rmax = fmaxf(rmax, fmaxf(fmaxf(fabsf(u[it].x), fabsf(u[it].y)), fmaxf(fabsf(u[it].z), fabsf(u[it].w))));
+    }
+  }
+  // one maximum per direction and workgroup, recorded on the workgroup's amax line
   if (do_rows || do_cols) {
-    const float wr = warp_max(rmax), wc = warp_max(cmax);
-    __syncthreads();
-    float* red = tile;
+    const uint32_t wr = wave_max_bits(rmax), wc = wave_max_bits(cmax);
     if (lane == 0) {
-      red[wave] = wr;
-      red[NT / 64 + wave] = wc;
+      red[0][wave] = wr;
+      red[1][wave] = wc;
     }
     __syncthreads();
     if (threadIdx.x < 2 && (threadIdx.x == 0 ? do_rows : do_cols)) {
-      float m = 0.0f;
+      uint32_t m = 0;
 #pragma unroll
-      for (int w = 0; w < NT / 64; ++w) m = fmaxf(m, red[threadIdx.x * (NT / 64) + w]);
-      amax_record(&g.sc[mat], threadIdx.x == 0 ? g.amax_row_slot : g.amax_col_slot, blockIdx.x, m);
+      for (int w = 0; w < NT / 64; ++w) m = m > red[threadIdx.x][w] ? m : red[threadIdx.x][w];
+      const float mf = g.amax_rotate ? 0.25f * __uint_as_float(m) : __uint_as_float(m);
+      amax_record(&g.sc[mat], threadIdx.x == 0 ? g.amax_row_slot : g.amax_col_slot, blockIdx.x, mf);
     }
   }
 }
