@@ -209,18 +209,18 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
 }
 
 // Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a
-// stage in binary32 when rho sigma < 2^44, see gemm_fp4.hip):
-//   rho = max_b n2_b 4^(e_b - e_min),  e = max(exponent field, 1) over blocks with
+// stage in binary32 when rho sigma < 2^48, see gemm_fp4.hip):
+//   rho = sum_b n2_b 4^(e_b - e_min),  e = max(exponent field, 1) over blocks with
 // a non-zero scale (a zero block adds nothing and does not lower e_min).
 FP4R_DEV uint32_t block_exp(uint32_t scale) {
   return (scale & 0x7Fu) ? max((scale >> 3) & 15u, 1u) : 15u;
 }
 FP4R_DEV float stage_rho(const uint32_t (&n2)[4], const uint32_t (&e)[4]) {
   const uint32_t emin = min(min(e[0], e[1]), min(e[2], e[3]));
-  float r = 0.0f;
+  double r = 0.0;
 #pragma unroll
-  for (int b = 0; b < 4; ++b) r = fmaxf(r, ldexpf((float)n2[b], 2 * (int)(e[b] - emin)));
-  return r;   // exact: n2 < 2^19 and the powers of two
+  for (int b = 0; b < 4; ++b) r += ldexp((double)n2[b], 2 * (int)(e[b] - emin));
+  return ru32(r);   // the sum is exact in binary64 (terms n2 < 2^19 times 4^k, k <= 14)
 }
 
 // The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3.

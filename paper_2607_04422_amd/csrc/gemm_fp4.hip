@@ -19,16 +19,18 @@
 // s = M 2^(e-10) (E4M3: M <= 15, e >= 1; subnormal scales as M = m, e = 1), so
 // every product of a row i of the first operand and a row j of the second over
 // a group G of blocks is a multiple of u = 2^(ea_min(i) + eb_min(j) - 22), the
-// minima over G.  By Cauchy-Schwarz, any partial sum of those products is at
-// most |G| sqrt(max_b T_a(i,b) max_b T_b(j,b)) in magnitude, T being a block's
-// sum of squared values.  With rho_i = max_b T_a(i,b) 2^(22 - 2 ea_min(i)) (and
-// sigma_j alike) the bound is below 2^24 u whenever |G|^2 rho_i sigma_j < 2^48;
-// then every partial sum is exactly representable in binary32, and the MFMAs
-// of the group may accumulate into one binary32 register, folded into binary64
-// once.  The encoder stores rho per stage and 16 rows, and each
-// compute wave tests the maxima over its own rows (diagonal tiles of symmetric
-// products test tile-wide maxima, so that (i, j) and (j, i) add the same
-// binary32 values in the same order and the product stays exactly symmetric).
+// minima over G.  Any partial sum of those products, in any order, is at most
+// their sum of magnitudes, and by Cauchy-Schwarz at most sqrt(T_a(i) T_b(j)),
+// T being the sum of squared values over G.  With rho_i = T_a(i) 2^(22 - 2 ea_min(i))
+// = sum_b n2_b 4^(e_b - ea_min(i)) (n2 = sum (2q)^2 M^2 per block; sigma_j alike)
+// the bound is below 2^24 u whenever rho_i sigma_j < 2^48; then every partial
+// sum is exactly representable in binary32, and the MFMAs of the group may
+// accumulate into one binary32 register, folded into binary64 once.  The encoder
+// stores rho per stage (four blocks) and 16 rows, rounded up to binary32, and
+// each compute wave tests the maxima over its own rows (diagonal tiles of
+// symmetric products test tile-wide maxima, so that (i, j) and (j, i) add the
+// same binary32 values in the same order and the product stays exactly
+// symmetric).
 #include "device.h"
 #include "internal.h"
 
@@ -382,9 +384,9 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     return rho_records_max(rec_a, g.M / 16, s, (int)(row0 / 16) + ga0, nga) *
            rho_records_max(rec_b, g.N / 16, s, (int)(col0 / 16) + gb0, ngb);
   };
-  // a stage chains as one group if 16 rho sigma < 2^48; the limit leaves room
-  // for the rounding of the binary32 product rho * sigma
-  constexpr float kLimStage = 17592186044416.0f * (1.0f - 1.0f / 65536.0f);   // 2^44 (1 - 2^-16)
+  // a stage chains as one group if rho sigma < 2^48; the limit leaves room for
+  // the rounding of the binary32 product rho * sigma
+  constexpr float kLimStage = 281474976710656.0f * (1.0f - 1.0f / 65536.0f);   // 2^48 (1 - 2^-16)
 #endif
 
   // stage -> LDS buffer `buf` (decoded operands)
