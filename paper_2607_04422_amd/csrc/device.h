@@ -98,10 +98,15 @@ FP4R_DEV E2m1Thresholds e2m1_thresholds(float r) {
   return th;
 }
 
+// The thresholds increase, so the count is found by bisection: bit 2 of the
+// index is a >= t3, bit 1 compares with t5 or t1, bit 0 with t6, t4, t2 or t0
+// (the comparison kinds, >= at odd and > at even positions, match each level).
 FP4R_DEV uint32_t e2m1_index_thr(float a, const E2m1Thresholds& th) {
-  return (uint32_t)(a > th.t[0]) + (uint32_t)(a >= th.t[1]) + (uint32_t)(a > th.t[2]) +
-         (uint32_t)(a >= th.t[3]) + (uint32_t)(a > th.t[4]) + (uint32_t)(a >= th.t[5]) +
-         (uint32_t)(a > th.t[6]);
+  const bool b2 = a >= th.t[3];
+  const bool b1 = a >= (b2 ? th.t[5] : th.t[1]);
+  const float lo = b1 ? th.t[2] : th.t[0], hi = b1 ? th.t[6] : th.t[4];
+  const bool b0 = a > (b2 ? hi : lo);
+  return (b2 ? 4u : 0u) | (b1 ? 2u : 0u) | (b0 ? 1u : 0u);
 }
 
 // Twice the E2M1 magnitude of an index: {0, 1, 2, 3, 4, 6, 8, 12} (one nibble each).
