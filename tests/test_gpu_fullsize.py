@@ -8,6 +8,8 @@
   on the whole batch (the same kernels and grids as the orthogonalisation); the
   oracle checks every stage of one batch member on sampled rows (quantisers,
   bit for bit) and sampled entries (products, to the binary32 value).
+* The 4096 x 4096 square case and the 3072 x 8192 / 8192 x 3072 pair: one traced
+  step each, checked the same way.
 * The stress case: the 8192 x 28672 matrix (one traced step) and end-to-end
   parity for a sample of its 256 512 x 512 companions.
 """
@@ -133,6 +135,26 @@ def test_bench_group_3072sq_step_stages():
     del mats, group
     a, b, c = F.fp4root_default_coeffs(3072, 3072, 5)[3]
     _check_traced_step(x0, 2, a, b, c, seed=5, step=3, label="3072x3072 x8")
+
+
+def test_square_4096_step_stages():
+    # one 4096 x 4096 Student-t matrix, square-shape coefficients (seed 1 inputs)
+    m = workloads.case_matrices("square_4096")[0]
+    x0 = ns.prepare(m)[0][None]
+    del m
+    a, b, c = F.fp4root_default_coeffs(4096, 4096, 5)[2]
+    _check_traced_step(np.ascontiguousarray(x0), 0, a, b, c, seed=1, step=2, label="4096x4096")
+
+
+def test_rect_pair_step_stages():
+    # 3072 x 8192 and 8192 x 3072 with lognormal row scales: both run short side first
+    # as one batch of two 3072 x 8192 matrices; member 1 is the tall one, transposed
+    mats = workloads.case_matrices("rect_3072x8192_pair")
+    assert mats[1].shape == (8192, 3072)
+    x0 = _canonical_batch(mats)
+    del mats
+    a, b, c = F.fp4root_default_coeffs(8192, 3072, 5)[0]
+    _check_traced_step(x0, 1, a, b, c, seed=2, step=0, label="8192x3072 (tall) in the pair")
 
 
 def test_stress_big_matrix_step_stages():
