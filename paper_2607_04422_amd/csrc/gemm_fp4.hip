@@ -497,13 +497,31 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 #else
   float st = kTable ? 0.0f : stage_bound(0);
   __syncthreads();
-  for (int s = 0; s < nstages; ++s) {
-    fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
-    fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-    compute(s & 1, blocks_in(s), kTable ? stage_bound(s) : st);
-    put((s & 1) ^ 1, sa, sb);
-    if (!kTable) st = stage_bound(s + 1);
-    __syncthreads();
+  if (kTable) {
+    // two stages per iteration, buffers as constants (measured faster for the
+    // symmetric products, slower for the update)
+    for (int s = 0; s < nstages; s += 2) {
+      fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
+      fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
+      compute(0, blocks_in(s), stage_bound(s));
+      put(1, sa, sb);
+      __syncthreads();
+      if (s + 1 >= nstages) break;
+      fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
+      fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
+      compute(1, blocks_in(s + 1), stage_bound(s + 1));
+      put(0, sa, sb);
+      __syncthreads();
+    }
+  } else {
+    for (int s = 0; s < nstages; ++s) {
+      fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
+      fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
+      compute(s & 1, blocks_in(s), st);
+      put((s & 1) ^ 1, sa, sb);
+      st = stage_bound(s + 1);
+      __syncthreads();
+    }
   }
   (void)na;
   (void)nb;
