@@ -228,8 +228,9 @@ FP4R_DEV float stage_rho(const uint32_t (&n2)[4], const uint32_t (&e)[4]) {
   return ru32(r);   // the sum is exact in binary64 (terms n2 < 2^19 times 4^k, k <= 14)
 }
 
-// The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3.
-FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e) {
+// The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3, and
+// (optionally) the row's e_min over the stage.
+FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e, uint32_t* emin = nullptr) {
   uint32_t qn[4], qe[4];
   const int base = (int)(threadIdx.x & 60u);
 #pragma unroll
@@ -237,7 +238,16 @@ FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e) {
     qn[k] = (uint32_t)__shfl((int)n2, base + k, 64);
     qe[k] = (uint32_t)__shfl((int)e, base + k, 64);
   }
+  if (emin) *emin = min(min(qe[0], qe[1]), min(qe[2], qe[3]));
   return stage_rho(qn, qe);
+}
+
+// rho of a row over two stages from each stage's (rho, e_min): the sums relative
+// to the smaller e_min, formed in binary64 and rounded up (the stage values are
+// already upper bounds).
+FP4R_DEV float pair_rho(float r0, uint32_t e0, float r1, uint32_t e1) {
+  const uint32_t e = min(e0, e1);
+  return ru32(ldexp((double)r0, 2 * (int)(e0 - e)) + ldexp((double)r1, 2 * (int)(e1 - e)));
 }
 
 // Maximum of non-negative values over the wave / over each 16 lanes.

@@ -34,6 +34,8 @@
 #include "device.h"
 #include "internal.h"
 
+#include <type_traits>
+
 namespace fp4r {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -113,15 +115,14 @@ struct Fp4Stage {
 
 // Where a thread's blocks come from: raw buffer resources over the tile's rows
 // of codes and scales (the hardware range check returns 0 for rows past the
-// matrix, so the tail tile needs no branch) and the thread's byte offsets at
-// stage 0.  Thread t stages row t / 4, block t % 4 of every 64-element stage.
+// matrix, so the tail tile needs no branch).  Thread t stages row t / 4, block
+// t % 4 of every 64-element stage: scale byte (t / 4) nkb + t % 4 + 4 s and the
+// codes at eight times that offset, the same offsets for both operands.
 constexpr int kBufWord3 = 0x00020000;          // raw 32-bit data format, no swizzle
 constexpr uint32_t kBufOutOfRange = 0x7FFFFFF0u;
 
 struct Fp4Src {
   __amdgpu_buffer_rsrc_t codes, scales;
-  uint32_t oc, os;
-  int kq;
 };
 
 template <int ROWS>
@@ -133,18 +134,18 @@ FP4R_DEV Fp4Src fp4_src(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t
       (void*)(op.codes + mat * op.codes_bstride + row0 * (K / 2)), (short)0, (int)(live * (K / 2)), kBufWord3);
   s.scales = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(op.scales + mat * op.scales_bstride + row0 * nkb), (short)0, (int)(live * nkb), kBufWord3);
-  const int r = threadIdx.x >> 2;
-  s.kq = threadIdx.x & 3;
-  s.oc = (uint32_t)(r * (K / 2) + s.kq * 8);
-  s.os = (uint32_t)(r * nkb + s.kq);
   return s;
 }
 
 template <int ROWS, int NT>
-FP4R_DEV void fp4_load(const Fp4Src& src, int64_t nkb, int stage, Fp4Stage<ROWS, NT>& s) {
-  const bool valid = (int64_t)stage * 4 + src.kq < nkb;   // blocks past the end of K read as 0
-  const uint32_t oc = valid ? src.oc + 32u * (uint32_t)stage : kBufOutOfRange;
-  const uint32_t os = valid ? src.os + 4u * (uint32_t)stage : kBufOutOfRange;
+FP4R_DEV void fp4_load(const Fp4Src& src, int nkb, int stage, Fp4Stage<ROWS, NT>& s) {
+  // blocks past the end of K read as 0 (nkb < 2^17; the block index is recomputed
+  // from the thread index, which is cheaper than keeping it live)
+  const int kq = (int)(threadIdx.x & 3);
+  const bool valid = stage * 4 + kq < nkb;
+  const uint32_t o = (threadIdx.x >> 2) * (uint32_t)nkb + (uint32_t)(kq + 4 * stage);
+  const uint32_t oc = valid ? 8u * o : kBufOutOfRange;
+  const uint32_t os = valid ? o : kBufOutOfRange;
   const auto c = __builtin_amdgcn_raw_buffer_load_b64(src.codes, (int)oc, 0, 0);
   s.codes[0] = make_uint2(c[0], c[1]);
   s.scales[0] = __builtin_amdgcn_raw_buffer_load_b8(src.scales, (int)os, 0, 0);
@@ -298,10 +299,6 @@ FP4R_DEV uint32_t wave_max_bits(float v) {
 #ifndef FP4R_FP4_WAVES_PER_EU
 #define FP4R_FP4_WAVES_PER_EU 4
 #endif
-// Stages in flight in registers ahead of the one in LDS (1 or 2).
-#ifndef FP4R_FP4_PREFETCH
-#define FP4R_FP4_PREFETCH 1
-#endif
 
 template <int MODE, int WM_, int WN_, int TM, int TN>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
@@ -316,7 +313,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   constexpr int kGa = BM / 16, kGb = BN / 16;   // 16-row groups per operand tile
   __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
   constexpr bool kTable = MODE != kModeUpdateX;   // record delivery (see above)
-  __shared__ float wbound[FP4R_FP4_CHAIN && kTable ? kRecStages : 1][NT / 64];
+  __shared__ uint8_t wflags[FP4R_FP4_CHAIN && kTable ? kRecStages : 1][NT / 64];
   __shared__ uint32_t red[2][NT / 64];   // per-wave amaxes (rows, columns)
   char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
   char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
@@ -327,7 +324,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN_, wn = wave % WN_;
-  const int64_t nkb = g.K / 16;
+  const int nkb = (int)(g.K / 16);   // K <= 2^21
   const int nstages = (int)((nkb + 3) / 4);
 
   double acc[TM][TN][16];
@@ -340,6 +337,9 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 
   const Fp4Src src_a = fp4_src<BM>(g.a, mat, g.M, g.K, row0);
   const Fp4Src src_b = fp4_src<BN>(g.b, mat, g.N, g.K, col0);
+  // a group chains if rho sigma < 2^48; the limit leaves room for the rounding of
+  // the binary32 product rho * sigma
+  constexpr float kLimStage = 281474976710656.0f * (1.0f - 1.0f / 65536.0f);   // 2^48 (1 - 2^-16)
 #if FP4R_FP4_CHAIN
   static_assert(kGa == kGb, "square tiles");
   // the rows a compute wave covers: TM * 2 loader groups of A, TN * 2 of B;
@@ -351,42 +351,44 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
   const float* rec_a = chain_on ? g.a.rhog + mat * g.a.rhog_bstride : nullptr;
   const float* rec_b = chain_on ? g.b.rhog + mat * g.b.rhog_bstride : nullptr;
-  // rho sigma of stages s0 .. s0 + kRecStages - 1 for this wave's rows into
-  // wbound[.][wave] (+inf without records or past the last stage; missing groups
-  // of a tail tile read 0: their rows are zero).  Only this wave touches its
-  // column, so no barrier is needed.
-  auto fill_bounds = [&](int s0) {
+  const float* rec8_a = chain_on && g.a.rho8 ? g.a.rho8 + mat * g.a.rho8_bstride : nullptr;
+  const float* rec8_b = chain_on && g.b.rho8 ? g.b.rho8 + mat * g.b.rho8_bstride : nullptr;
+  // the largest record over groups g0 .. g0 + ng - 1 of record row `idx`
+  // (missing groups of a tail tile read 0: their rows are zero)
+  auto group_max = [&](const float* rec, int64_t groups_all, int64_t idx, int64_t g0, int ng) {
+    float mx = 0.0f;
+    for (int k = 0; k < ng; ++k)
+      if (g0 + k < groups_all) mx = fmaxf(mx, rec[idx * groups_all + g0 + k]);
+    return mx;
+  };
+  // chain flags of stages s0 .. s0 + kRecStages - 1 for this wave's rows into
+  // wflags[.][wave] (one stage per lane): bit 0 = the stage chains, bit 1 (even
+  // stages) = the stage and the next chain as one group.  Only this wave touches
+  // its column, so no barrier is needed.
+  auto fill_flags = [&](int s0) {
     if (!kTable) return;
     const int64_t nga_all = g.M / 16, ngb_all = g.N / 16;
+    const int64_t a0 = row0 / 16 + ga0, b0 = col0 / 16 + gb0;
 #pragma unroll
     for (int h = 0; h < kRecStages / 64; ++h) {
       const int ss = lane + 64 * h;
       const int64_t sg = (int64_t)s0 + ss;
-      float v = __builtin_inff();
+      uint32_t f = 0;
       if (chain_on && sg < nstages) {
-        float ma = 0.0f, mb = 0.0f;
-        for (int k = 0; k < nga; ++k) {
-          const int64_t grp = row0 / 16 + ga0 + k;
-          if (grp < nga_all) ma = fmaxf(ma, rec_a[sg * nga_all + grp]);
-        }
-        for (int k = 0; k < ngb; ++k) {
-          const int64_t grp = col0 / 16 + gb0 + k;
-          if (grp < ngb_all) mb = fmaxf(mb, rec_b[sg * ngb_all + grp]);
-        }
-        v = ma * mb;
+        if (group_max(rec_a, nga_all, sg, a0, nga) * group_max(rec_b, ngb_all, sg, b0, ngb) < kLimStage) f |= 1u;
+        if (rec8_a && rec8_b && (sg & 1) == 0 && sg + 1 < nstages &&
+            group_max(rec8_a, nga_all, sg / 2, a0, nga) * group_max(rec8_b, ngb_all, sg / 2, b0, ngb) < kLimStage)
+          f |= 2u;
       }
-      wbound[ss][wave] = v;
+      wflags[ss][wave] = (uint8_t)f;
     }
   };
+  auto stage_flags = [&](int s) { return (uint32_t)wflags[s % kRecStages][wave]; };
   auto stage_bound = [&](int s) {
-    if (kTable) return wbound[s % kRecStages][wave];
     if (!chain_on || s >= nstages) return __builtin_inff();
     return rho_records_max(rec_a, g.M / 16, s, (int)(row0 / 16) + ga0, nga) *
            rho_records_max(rec_b, g.N / 16, s, (int)(col0 / 16) + gb0, ngb);
   };
-  // a stage chains as one group if rho sigma < 2^48; the limit leaves room for
-  // the rounding of the binary32 product rho * sigma
-  constexpr float kLimStage = 281474976710656.0f * (1.0f - 1.0f / 65536.0f);   // 2^48 (1 - 2^-16)
 #endif
 
   // stage -> LDS buffer `buf` (decoded operands)
@@ -396,17 +398,19 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   };
 
   const f32x16 zero = {};
-  // MFMAs and binary64 folds of the stage in LDS buffer `buf` (kbs blocks)
-  auto compute = [&](int buf, int kbs, float st) {
+  f32x16 p[TM][TN];   // the binary32 chain registers
+  // MFMAs and binary64 folds of the stage in LDS buffer `buf` (kbs blocks).  fl:
+  // bit k - 1 set = block k accumulates onto block k - 1 (blocks past the end of K
+  // are zero in LDS and join any group).  Odd stages (odd_tag true) start on the
+  // chain registers as left by the previous stage; fold_end folds the registers
+  // at the end, and even stages then clear them for the odd stage after them.
+  auto compute = [&](auto odd_tag, int buf, int kbs, uint32_t fl, bool fold_end) {
+    constexpr bool ODD = decltype(odd_tag)::value;
     if (kbs <= 0) return;
     const char* la = lds_a[buf];
     const char* lb = lds_b[buf];
 #if FP4R_FP4_CHAIN
-    // chain flags: bit k - 1 set = block k accumulates onto block k - 1 (blocks
-    // past the end of K are zero in LDS and join any group)
-    const uint32_t fl = st < kLimStage ? 7u : 0u;
     // the TM x TN tiles' chains run interleaved, block by block
-    f32x16 p[TM][TN];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       f16x8 av[TM], bv[TN];
@@ -418,7 +422,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
       for (int j = 0; j < TN; ++j)
         bv[j] = *reinterpret_cast<const f16x8*>(
             lb + lds_kb_base<BN>(kb) + lds_row_off((wn * TN + j) * 32 + (lane & 31), lane >> 5));
-      const bool chained = kb > 0 && ((fl >> (kb - 1)) & 1u);
+      const bool chained = kb > 0 ? ((fl >> (kb - 1)) & 1u) != 0 : ODD;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -431,13 +435,18 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
         }
       __builtin_amdgcn_sched_barrier(0);   // keep operand loads next to their use
     }
+    if (fold_end) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
+          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
+          if (!ODD) p[i][j] = zero;
+        }
+    }
 #else
+    (void)fl; (void)fold_end;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if (kb >= kbs) break;
@@ -461,71 +470,47 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     }
 #endif
   };
-  auto blocks_in = [&](int s) { return (int)(nkb - (int64_t)s * 4 < 4 ? nkb - (int64_t)s * 4 : 4); };
+  auto blocks_in = [&](int s) { return nkb - s * 4 < 4 ? nkb - s * 4 : 4; };
 
-  Fp4Stage<BM, NT> sa, na;
-  Fp4Stage<BN, NT> sb, nb;
+  Fp4Stage<BM, NT> sa;
+  Fp4Stage<BN, NT> sb;
   fp4_load<BM, NT>(src_a, nkb, 0, sa);
   fp4_load<BN, NT>(src_b, nkb, 0, sb);
   put(0, sa, sb);
-  if (FP4R_FP4_CHAIN) fill_bounds(0);
-#if FP4R_FP4_PREFETCH == 2
-  // Stage s is computed from LDS while stage s + 1 waits in one register set and
-  // stage s + 2 loads into the other; the loop body runs two stages with the
-  // sets swapped, so no register copy waits on a load in flight.
-  fp4_load<BM, NT>(src_a, nkb, 1, sa);
-  fp4_load<BN, NT>(src_b, nkb, 1, sb);
+  if (FP4R_FP4_CHAIN) fill_flags(0);
   __syncthreads();
-  float st = kTable ? 0.0f : stage_bound(0);
-  auto step = [&](int s, int buf, Fp4Stage<BM, NT>& ha, Fp4Stage<BN, NT>& hb, Fp4Stage<BM, NT>& la2,
-                  Fp4Stage<BN, NT>& lb2) {
-    // unconditional: past the last stage every offset is out of range and reads 0,
-    // and a branch here would make the waits below cover these loads too
-    fp4_load<BM, NT>(src_a, nkb, s + 2, la2);
-    fp4_load<BN, NT>(src_b, nkb, s + 2, lb2);
-    compute(buf, blocks_in(s), kTable ? stage_bound(s) : st);
-    put(buf ^ 1, ha, hb);
-    if (!kTable) st = stage_bound(s + 1);
-    __syncthreads();
-  };
-  // no data-dependent branch in the loop body (a stage past the end computes
-  // nothing and stages zeros), so the load waits stay exact
-  for (int s = 0; s < nstages; s += 2) {
-    step(s, 0, sa, sb, na, nb);
-    step(s + 1, 1, na, nb, sa, sb);
-  }
-#else
-  float st = kTable ? 0.0f : stage_bound(0);
-  __syncthreads();
+  // Stage s is computed from LDS buffer s % 2 while stage s + 1 loads into
+  // registers; it is decoded into the other buffer after the MFMAs.
   if (kTable) {
-    // two stages per iteration, buffers as constants (measured faster for the
-    // symmetric products, slower for the update)
+    // two stages per iteration, buffers as constants; a stage pair may chain as
+    // one group of eight blocks (one fold per 128 elements)
     for (int s = 0; s < nstages; s += 2) {
+      const uint32_t f0 = FP4R_FP4_CHAIN ? stage_flags(s) : 0u;
+      const bool pair = (f0 & 2u) != 0, has_odd = s + 1 < nstages;
       fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
       fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-      compute(0, blocks_in(s), stage_bound(s));
+      compute(std::false_type(), 0, blocks_in(s), (pair || (f0 & 1u)) ? 7u : 0u, !pair);
       put(1, sa, sb);
       __syncthreads();
-      if (s + 1 >= nstages) break;
+      if (!has_odd) break;
+      const uint32_t f1 = FP4R_FP4_CHAIN ? stage_flags(s + 1) : 0u;
       fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
       fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
-      compute(1, blocks_in(s + 1), stage_bound(s + 1));
+      compute(std::true_type(), 1, blocks_in(s + 1), (pair || (f1 & 1u)) ? 7u : 0u, true);
       put(0, sa, sb);
       __syncthreads();
     }
   } else {
+    float st = FP4R_FP4_CHAIN ? stage_bound(0) : 0.0f;
     for (int s = 0; s < nstages; ++s) {
       fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
       fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-      compute(s & 1, blocks_in(s), st);
+      compute(std::false_type(), s & 1, blocks_in(s), st < kLimStage ? 7u : 0u, true);
       put((s & 1) ^ 1, sa, sb);
-      st = stage_bound(s + 1);
+      if (FP4R_FP4_CHAIN) st = stage_bound(s + 1);
       __syncthreads();
     }
   }
-  (void)na;
-  (void)nb;
-#endif
 
   // epilogue: binary64 formula, one rounding to binary32, staged through LDS
   // (the main loop's buffers are free after the last barrier)

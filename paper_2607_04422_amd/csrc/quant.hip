@@ -445,7 +445,11 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   uint32_t n2;
   quant_block(u, sg, adaptive != 0, scale, codes, n2);
   if (want_rho) {
-    const float rho = wave_max_pos(quad_stage_rho(n2, block_exp(scale)));
+    uint32_t emin;
+    const float rrow = quad_stage_rho(n2, block_exp(scale), &emin);
+    if (out.rowst && (threadIdx.x & 3) == 0)
+      out.rowst[b * out.rowst_bstride + (c / 64) * in.rows + r] = make_uint2(__float_as_uint(rrow), emin);
+    const float rho = wave_max_pos(rrow);
     if ((threadIdx.x & 63) == 0)
       out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
   }
@@ -512,7 +516,11 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
     // chain record of this wave's 16 rows for the tile's 64-column stage: lanes
     // 4i .. 4i + 3 hold row i's four blocks (blocks past the edge count as zero)
     if (qx.rhog) {
-      const float rho = wave_max_pos(quad_stage_rho(n2, e));
+      uint32_t emin;
+      const float rrow = quad_stage_rho(n2, e, &emin);
+      if (qx.rowst && (threadIdx.x & 3) == 0 && r < m)
+        qx.rowst[b * qx.rowst_bstride + (c0 / 64) * m + r] = make_uint2(__float_as_uint(rrow), emin);
+      const float rho = wave_max_pos(rrow);
       if ((threadIdx.x & 63) == 0 && r0 + 16 * (threadIdx.x >> 6) < m)
         qx.rhog[b * qx.rhog_bstride + (c0 / 64) * (m / 16) + (r0 / 16) + (threadIdx.x >> 6)] = rho;
     }
@@ -556,6 +564,35 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       }
     }
   }
+}
+
+// One thread per (stage pair, 16 rows) of a matrix.
+__global__ __launch_bounds__(256) void k_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_t rows,
+                                                      int64_t npairs, float* rho8, int64_t rho8_bstride) {
+  const int64_t b = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t groups = rows / 16;
+  if (t >= npairs * groups) return;
+  const int64_t pr = t / groups, gr = t % groups;
+  const uint2* s0 = rowst + b * rowst_bstride + (2 * pr) * rows + 16 * gr;
+  const uint2* s1 = s0 + rows;
+  float m = 0.0f;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const uint2 a = s0[i], c = s1[i];
+    m = fmaxf(m, pair_rho(__uint_as_float(a.x), a.y, __uint_as_float(c.x), c.y));
+  }
+  rho8[b * rho8_bstride + pr * groups + gr] = m;
+}
+
+hipError_t launch_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_t batch, int64_t rows,
+                               int64_t nstages, float* rho8, int64_t rho8_bstride, hipStream_t st) {
+  const int64_t n = (nstages / 2) * (rows / 16);
+  if (n == 0 || batch == 0) return hipSuccess;
+  const dim3 grid((uint32_t)((n + 255) / 256), (uint32_t)batch);
+  hipLaunchKernelGGL(k_pair_records, grid, dim3(256), 0, st, rowst, rowst_bstride, rows, nstages / 2, rho8,
+                     rho8_bstride);
+  return hipGetLastError();
 }
 
 hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
