@@ -556,9 +556,29 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
         val[i][j][e] = in ? (float)v : 0.0f;
         tile[rl * kLdT + cl] = val[i][j][e];
       }
-  // off-diagonal tiles of symmetric products: the transposed tile straight from
-  // registers (four consecutive rows of a column form a row segment of it)
+  // off-diagonal tiles of symmetric products (and a transposed final output): the
+  // transposed tile straight from registers (four consecutive rows of a column
+  // form a row segment of it)
   const bool mirror = kSym && tm != tn;
+  const bool fin = !kSym && g.fin_count > 0;
+  float* const fin_out = fin ? g.fin_out[mat] : nullptr;
+  const int64_t fin_ld = fin ? g.fin_ld[mat] : 0;
+  const bool fin_tall = fin && g.fin_tall[mat] != 0;
+  if (fin_tall) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int rb = (wm * TM + i) * 32 + 8 * e4 + 4 * (lane >> 5);
+          const int cl = (wn * TN + j) * 32 + (lane & 31);
+          const int64_t ur = col0 + cl, uc = row0 + rb;
+          if (ur < g.N && uc < g.M)
+            *reinterpret_cast<float4*>(fin_out + ur * fin_ld + uc) =
+                make_float4(val[i][j][4 * e4], val[i][j][4 * e4 + 1], val[i][j][4 * e4 + 2], val[i][j][4 * e4 + 3]);
+        }
+  }
   if (mirror) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -625,7 +645,8 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     for (int it = 0; it < kIt; ++it) {
       const int idx = threadIdx.x + NT * it;
       const int64_t r = row0 + idx / kSlots, c = col0 + 4 * (idx % kSlots);
-      if (r < g.M && c < g.N) *reinterpret_cast<float4*>(out + r * g.N + c) = u[it];
+      if (r < g.M && c < g.N && !fin_tall)
+        *reinterpret_cast<float4*>(fin ? fin_out + r * fin_ld + c : out + r * g.N + c) = u[it];
     }
     if (do_rows && g.amax_rotate) {
 #pragma unroll

@@ -170,6 +170,13 @@ struct GemmFp4Args {
   int64_t out_bstride;
   const float* aux;       // kModeGramB: A (may equal out); kModeUpdateX: X_k (may equal out)
   float ca, cb, cc;
+  // kModeUpdateX, last step: when fin_count > 0 the output goes to the callers'
+  // matrices instead of `out`: matrix b to fin_out[b] with row stride fin_ld[b],
+  // transposed (fin_out[b][c][r] = X[r][c]) when fin_tall[b]
+  int fin_count = 0;
+  float* fin_out[kMaxChunk] = {};
+  int64_t fin_ld[kMaxChunk] = {};
+  uint8_t fin_tall[kMaxChunk] = {};
 };
 
 // NVFP4 product with exact block sums accumulated in binary64.
