@@ -122,6 +122,63 @@ struct BlockCand {
   double half_ss;   // 0.5 s s_g, exact
 };
 
+// Codes and error sums of a candidate whose scale rs = s s_g is positive, with the
+// E2M1 rounding done by the hardware conversion (round to nearest even, saturating,
+// sign kept) on y = u * r, r ~ 1/rs.  fl32(u / rs) lies strictly between y
+// computed with r (1 - 2^-19) and with r (1 + 2^-19) (r is within 2^-23 of 1/rs,
+// each product within 2^-24), and the rounding is monotone, so when both bracket
+// values give the same codes, fl32(u / rs) gives them too.  Returns false when the
+// codes differ (an element lies next to a grid midpoint) or r is not finite.
+FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
+  const float rinv = __builtin_amdgcn_rcpf(rs);
+  if (!(rinv < 1e38f)) return false;
+  const float rup = rinv * (1.0f + 0x1p-19f), rdn = rinv * (1.0f - 0x1p-19f);
+  uint32_t c[2] = {0u, 0u}, cu[2] = {0u, 0u}, cd[2] = {0u, 0u};
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int w = k >> 2;
+    const float a = u[2 * k], b = u[2 * k + 1];
+    switch (k & 3) {
+#define FP4R_CVT(SEL)                                                                   \
+  case SEL:                                                                             \
+    c[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c[w], a * rinv, b * rinv, 1.0f, SEL); \
+    cu[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(cu[w], a * rup, b * rup, 1.0f, SEL); \
+    cd[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(cd[w], a * rdn, b * rdn, 1.0f, SEL); \
+    break;
+      FP4R_CVT(0)
+      FP4R_CVT(1)
+      FP4R_CVT(2)
+      FP4R_CVT(3)
+#undef FP4R_CVT
+    }
+  }
+  if (c[0] != cu[0] || c[0] != cd[0] || c[1] != cu[1] || c[1] != cd[1]) return false;
+  r.codes = (uint64_t)c[0] | ((uint64_t)c[1] << 32);
+  // decoded values q (= tw / 2, signed) back from the codes; u - q rs has the
+  // magnitude of |u| - tw (rs / 2), so the sum equals the element-order fma sum
+  float err = 0.0f, k2 = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int w = k >> 2;
+    float2 q;
+    switch (k & 3) {
+      case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c[w], 1.0f, 0)); break;
+      case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c[w], 1.0f, 1)); break;
+      case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c[w], 1.0f, 2)); break;
+      default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c[w], 1.0f, 3)); break;
+    }
+    const float d0 = fmaf(-q.x, rs, u[2 * k]);
+    err = fmaf(d0, d0, err);
+    const float d1 = fmaf(-q.y, rs, u[2 * k + 1]);
+    err = fmaf(d1, d1, err);
+    k2 = fmaf(q.x, q.x, k2);
+    k2 = fmaf(q.y, q.y, k2);
+  }
+  r.err = err;
+  r.k2 = (uint32_t)(4.0f * k2);   // exact: sums of q^2 are multiples of 1/4 below 2^10
+  return true;
+}
+
 FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M) {
   BlockCand r;
   const float den = M * sg;
@@ -134,7 +191,12 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   r.codes = 0;
   r.err = 0.0f;
   r.k2 = 0;
+  if (rs > 0.0f && quant_candidate_hw(u, rs, r)) return r;
   if (rs > 0.0f) {
+    // elements next to a grid midpoint: the exact threshold comparisons
+    r.codes = 0;
+    r.err = 0.0f;
+    r.k2 = 0;
     const E2m1Thresholds th = e2m1_thresholds(rs);
     const float h = 0.5f * rs;
 #pragma unroll
