@@ -132,3 +132,33 @@ def test_quantize_adaptive_near_ties():
         codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=axis, flags=F.F_ADAPTIVE46, seed=0)
         ref = quantize(m, axis, None, True)
         assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"near ties axis={axis}")
+
+
+def test_quantize_grid_midpoints():
+    """Elements exactly on E2M1 grid midpoints of their block (ties to the even code)
+    and a few ulps to either side: the hardware-rounded fast path must hand these
+    blocks to the exact threshold comparisons and match the reference bit for bit."""
+    rng = np.random.default_rng(5)
+    rows, cols = 48, 256
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0], np.float32)
+    m = np.zeros((rows, cols), np.float32)
+    for r in range(rows):
+        for b in range(cols // 16):
+            blk = m[r, 16 * b:16 * b + 16]
+            s = np.float32(rng.choice([1.0, 1.125, 1.5, 1.875]) * 2.0 ** int(rng.integers(-8, 6)))
+            blk[0] = np.float32(6.0) * s                    # block maximum: the M = 6 scale is s
+            v = mids[rng.integers(0, 7, 15)] * s             # exact: at most 7 significant bits
+            steps = rng.integers(-3, 4, 15)
+            for i in range(15):
+                x = v[i]
+                for _ in range(abs(int(steps[i]))):
+                    x = np.nextafter(x, np.float32(np.inf if steps[i] > 0 else -np.inf), dtype=np.float32)
+                blk[1 + i] = x
+            blk[:] *= rng.choice([-1.0, 1.0], 16).astype(np.float32)
+    m[0, 0] = 2688.0                                        # s_g = 1
+    x = torch.from_numpy(m).cuda()
+    for flags in (0, F.F_ADAPTIVE46):
+        for axis in (1, 0):
+            codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=axis, flags=flags, seed=0)
+            ref = quantize(m, axis, None, bool(flags & F.F_ADAPTIVE46))
+            assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"midpoints flags={flags} axis={axis}")
