@@ -23,10 +23,18 @@ constexpr float kSgDivisor = 2688.0f;
 // A row block x becomes x diag(d) H / 4; a column block y becomes
 // H diag(d) y / 4, the transpose of the same map.  (Sections 2, 3.4.)
 FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
+  // signs and the stride-1 stage together: fl(s_i u_i +- s_j u_j) as one fma of
+  // exact products (the signs are uniform, so s_i costs no vector work)
 #pragma unroll
-  for (int i = 0; i < 16; ++i) u[i] = __uint_as_float(__float_as_uint(u[i]) ^ (((mask >> i) & 1u) << 31));
+  for (int i = 0; i < 16; i += 2) {
+    const float si = ((mask >> i) & 1u) ? -1.0f : 1.0f, sj = ((mask >> (i + 1)) & 1u) ? -1.0f : 1.0f;
+    const float t = sj * u[i + 1];
+    const float p = fmaf(si, u[i], t), q = fmaf(si, u[i], -t);
+    u[i] = p;
+    u[i + 1] = q;
+  }
 #pragma unroll
-  for (int h = 1; h < 16; h <<= 1) {
+  for (int h = 2; h < 16; h <<= 1) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if ((i & h) == 0) {
