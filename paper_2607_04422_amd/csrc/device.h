@@ -48,6 +48,36 @@ FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
   for (int i = 0; i < 16; ++i) u[i] *= 0.25f;
 }
 
+// The largest magnitude over a block after rotate16, times 4: the same butterfly
+// up to the last stage, whose pair (fl(p + q), fl(p - q)) has the larger magnitude
+// fl(|p| + |q|).  Multiplying the result by 1/4 gives max |rotate16(u)| exactly
+// (rounding is monotone, so the factor commutes with the maximum).
+FP4R_DEV float rot16_absmax4(float (&u)[16], uint32_t mask) {
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) {
+    const float si = ((mask >> i) & 1u) ? -1.0f : 1.0f, sj = ((mask >> (i + 1)) & 1u) ? -1.0f : 1.0f;
+    const float t = sj * u[i + 1];
+    const float p = fmaf(si, u[i], t), q = fmaf(si, u[i], -t);
+    u[i] = p;
+    u[i + 1] = q;
+  }
+#pragma unroll
+  for (int h = 2; h < 8; h <<= 1) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if ((i & h) == 0) {
+        const float p = u[i], q = u[i + h];
+        u[i] = p + q;
+        u[i + h] = p - q;
+      }
+    }
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(u[i]) + fabsf(u[i + 8]));
+  return m;
+}
+
 // E4M3FN code of v in [0, 448], round to nearest, ties to the even code.
 FP4R_DEV uint32_t e4m3_rne(float v) {
   if (v < 0.015625f) {                           // below 2^-6: grid m * 2^-9, m = 0..8

@@ -277,9 +277,12 @@ __global__ __launch_bounds__(256) void k_prep_copy(MatChunk ch, MatScalars* sc, 
       float u[16];
 #pragma unroll
       for (int k = 0; k < 16; ++k) u[k] = tile[i][16 * b + k];
-      if (rotate) rotate16(u, mask);
+      if (rotate) {
+        mr = 0.25f * rot16_absmax4(u, mask);
+      } else {
 #pragma unroll
-      for (int k = 0; k < 16; ++k) mr = fmaxf(mr, fabsf(u[k]));
+        for (int k = 0; k < 16; ++k) mr = fmaxf(mr, fabsf(u[k]));
+      }
     }
   }
   {
@@ -288,9 +291,12 @@ __global__ __launch_bounds__(256) void k_prep_copy(MatChunk ch, MatScalars* sc, 
       float u[16];
 #pragma unroll
       for (int k = 0; k < 16; ++k) u[k] = tile[16 * b + k][j];
-      if (rotate) rotate16(u, mask);
+      if (rotate) {
+        mc = 0.25f * rot16_absmax4(u, mask);
+      } else {
 #pragma unroll
-      for (int k = 0; k < 16; ++k) mc = fmaxf(mc, fabsf(u[k]));
+        for (int k = 0; k < 16; ++k) mc = fmaxf(mc, fabsf(u[k]));
+      }
     }
   }
   const float br = block_max_256(mr, red);
@@ -394,9 +400,12 @@ __global__ __launch_bounds__(256) void k_amax(Batch in, uint32_t mask, int rotat
 #pragma unroll
       for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
     }
-    if (rotate) rotate16(u, mask);
+    if (rotate) {
+      m = 0.25f * rot16_absmax4(u, mask);
+    } else {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(u[i]));
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(u[i]));
+    }
     if (!ok) m = 0.0f;
   }
   m = warp_max(m);
