@@ -483,25 +483,32 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   // registers; it is decoded into the other buffer after the MFMAs.
   if (kTable) {
     // two stages per iteration, buffers as constants; a stage pair may chain as
-    // one group of eight blocks (one fold per 128 elements)
+    // one group of eight blocks (one fold per 128 elements); the last stage loads
+    // and decodes nothing
     for (int s = 0; s < nstages; s += 2) {
       const uint32_t f0 = FP4R_FP4_CHAIN ? stage_flags(s) : 0u;
       const bool pair = (f0 & 2u) != 0, has_odd = s + 1 < nstages;
-      fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
-      fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
+      if (has_odd) {
+        fp4_load<BM, NT>(src_a, nkb, s + 1, sa);
+        fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
+      }
       compute(std::false_type(), 0, blocks_in(s), (pair || (f0 & 1u)) ? 7u : 0u, !pair);
-      put(1, sa, sb);
+      if (has_odd) put(1, sa, sb);
       __syncthreads();
       if (!has_odd) break;
       const uint32_t f1 = FP4R_FP4_CHAIN ? stage_flags(s + 1) : 0u;
-      fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
-      fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
+      const bool more = s + 2 < nstages;
+      if (more) {
+        fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
+        fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
+      }
       compute(std::true_type(), 1, blocks_in(s + 1), (pair || (f1 & 1u)) ? 7u : 0u, true);
-      put(0, sa, sb);
+      if (more) put(0, sa, sb);
       __syncthreads();
     }
   } else {
     float st = FP4R_FP4_CHAIN ? stage_bound(0) : 0.0f;
+    // (unconditional loads and stores past the last stage: measured faster here)
     for (int s = 0; s < nstages; ++s) {
       fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
       fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
