@@ -154,10 +154,9 @@ FP4R_DEV uint32_t e2m1_twice(uint32_t idx) { return (0xC8643210u >> (idx << 2)) 
 struct BlockCand {
   uint32_t scale;   // E4M3 code
   uint64_t codes;   // 16 nibbles, element i in bits 4i..4i+3
-  uint32_t k2;      // sum of (2 q)^2 over the block: twice-magnitudes squared
   float err;        // sum of squared decode errors in binary32 (fma, element order)
   float s2;         // (s s_g)^2 in binary32, for the error bound
-  double half_ss;   // 0.5 s s_g, exact
+  float s;          // the E4M3 scale value
 };
 
 // Codes and error sums of a candidate whose scale rs = s s_g is positive, with the
@@ -194,7 +193,7 @@ FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
   r.codes = (uint64_t)c[0] | ((uint64_t)c[1] << 32);
   // decoded values q (= tw / 2, signed) back from the codes; u - q rs has the
   // magnitude of |u| - tw (rs / 2), so the sum equals the element-order fma sum
-  float err = 0.0f, k2 = 0.0f;
+  float err = 0.0f;
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     const int w = k >> 2;
@@ -209,11 +208,8 @@ FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
     err = fmaf(d0, d0, err);
     const float d1 = fmaf(-q.y, rs, u[2 * k + 1]);
     err = fmaf(d1, d1, err);
-    k2 = fmaf(q.x, q.x, k2);
-    k2 = fmaf(q.y, q.y, k2);
   }
   r.err = err;
-  r.k2 = (uint32_t)(4.0f * k2);   // exact: sums of q^2 are multiples of 1/4 below 2^10
   return true;
 }
 
@@ -224,17 +220,15 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
   r.scale = e4m3_rne(v);
   const float s = e4m3_value(r.scale);
   const float rs = s * sg;
-  r.half_ss = 0.5 * ((double)s * (double)sg);   // exact: 4 + 24 significant bits
+  r.s = s;
   r.s2 = rs * rs;
   r.codes = 0;
   r.err = 0.0f;
-  r.k2 = 0;
   if (rs > 0.0f && quant_candidate_hw(u, rs, r)) return r;
   if (rs > 0.0f) {
     // elements next to a grid midpoint: the exact threshold comparisons
     r.codes = 0;
     r.err = 0.0f;
-    r.k2 = 0;
     const E2m1Thresholds th = e2m1_thresholds(rs);
     const float h = 0.5f * rs;
 #pragma unroll
@@ -244,7 +238,6 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
       const uint32_t idx = e2m1_index_thr(a, th);
       r.codes |= (uint64_t)((neg << 3) | idx) << (4 * i);
       const uint32_t tw = e2m1_twice(idx);
-      r.k2 += tw * tw;
       const float d = fmaf(-(float)tw, h, a);
       r.err = fmaf(d, d, r.err);
     }
@@ -261,21 +254,22 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
 
 // The candidate's squared error in binary64, summed in element order: the
 // reference definition of the 4/6 choice.
-FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c) {
+FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c, float sg) {
+  const double half_ss = 0.5 * ((double)c.s * (double)sg);   // exact: 4 + 24 significant bits
   double e = 0.0;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const double dec = (double)e2m1_twice((uint32_t)(c.codes >> (4 * i)) & 7u) * c.half_ss;
+    const double dec = (double)e2m1_twice((uint32_t)(c.codes >> (4 * i)) & 7u) * half_ss;
     const double d = (double)fabsf(u[i]) - dec;   // exact; d^2 as for the signed difference
     e = e + d * d;
   }
   return e;
 }
 
-// Quantise one (already rotated) block given the tensor scale.  `n2` receives
-// sum_i (2 q_i)^2 M^2 with M the scale's integer significand (8..15, or the
-// mantissa of a subnormal scale): the block's sum of squared decoded values is
-// n2 2^(2 e - 22), e = max(exponent field, 1).
+// Quantise one (already rotated) block given the tensor scale.  With want_n2,
+// `n2` receives sum_i (2 q_i)^2 M^2 with M the scale's integer significand (8..15,
+// or the mantissa of a subnormal scale): the block's sum of squared decoded values
+// is n2 2^(2 e - 22), e = max(exponent field, 1); otherwise n2 is 0.
 //
 // Adaptive 4/6 keeps M = 4 iff its binary64 squared error is strictly smaller.
 // The binary32 sums decide when they are far apart: with S = s s_g, decoded
@@ -285,7 +279,7 @@ FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c) {
 // If err4 + 2 (B4 + B6) < err6 the exact E4 < E6 by more than any binary64
 // rounding, and symmetrically; otherwise both are recomputed in binary64.
 FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_t& scale,
-                          uint64_t& codes, uint32_t& n2) {
+                          uint64_t& codes, uint32_t& n2, bool want_n2 = true) {
   n2 = 0;
   if (sg == 0.0f) {   // all-zero tensor: zero scales, zero magnitudes, signs kept
     codes = 0;
@@ -304,13 +298,29 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
     bool use4;
     if (c4.err + b < c6.err) use4 = true;
     else if (c6.err + b < c4.err) use4 = false;
-    else use4 = cand_err64(u, c4) < cand_err64(u, c6);
+    else use4 = cand_err64(u, c4, sg) < cand_err64(u, c6, sg);
     if (use4) c6 = c4;
   }
   scale = c6.scale;
   codes = c6.codes;
+  if (!want_n2) return;
+  // sum of q^2 from the decoded codes (exact: multiples of 1/4 below 2^10)
+  const uint32_t w[2] = {(uint32_t)codes, (uint32_t)(codes >> 32)};
+  float k2 = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float2 q;
+    switch (k & 3) {
+      case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 0)); break;
+      case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 1)); break;
+      case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 2)); break;
+      default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 3)); break;
+    }
+    k2 = fmaf(q.x, q.x, k2);
+    k2 = fmaf(q.y, q.y, k2);
+  }
   const uint32_t mant = (scale >> 3) ? 8u + (scale & 7u) : (scale & 7u);
-  n2 = c6.k2 * mant * mant;
+  n2 = (uint32_t)(4.0f * k2) * mant * mant;
 }
 
 // Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a

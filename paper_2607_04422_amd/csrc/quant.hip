@@ -452,7 +452,7 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   uint32_t scale;
   uint64_t codes;
   uint32_t n2;
-  quant_block(u, sg, adaptive != 0, scale, codes, n2);
+  quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho);
   if (want_rho) {
     uint32_t emin;
     const float rrow = quad_stage_rho(n2, block_exp(scale), &emin);
@@ -516,7 +516,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       if (rotate) rotate16(u, mask);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgn, adaptive != 0, scale, codes, n2);
+      quant_block(u, sgn, adaptive != 0, scale, codes, n2, qx.rhog != nullptr);
       e = block_exp(scale);
       *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + r * (n / 2) + c / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
@@ -545,7 +545,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       if (rotate) rotate16(u, mask);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgm, adaptive != 0, scale, codes, n2);
+      quant_block(u, sgm, adaptive != 0, scale, codes, n2, qxt.rhog != nullptr);
       e = block_exp(scale);
       *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + c * (m / 2) + r / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
