@@ -18,16 +18,23 @@ namespace fp4r {
 // s_g = amax / (6 * 448): the largest block scale maps to the largest E4M3.
 constexpr float kSgDivisor = 2688.0f;
 
+// -1.0f where bit i of mask is set, else 1.0f (integer operations only, so a
+// uniform mask gives a scalar value).
+FP4R_DEV float sign_factor(uint32_t mask, int i) {
+  return __uint_as_float(0x3F800000u | (((mask >> i) & 1u) << 31));
+}
+
 // Random 16x16 Hadamard: flip the signs selected by `mask` (bit i set means
 // d_i = -1), then the Sylvester butterfly with strides 1, 2, 4, 8, then * 1/4.
 // A row block x becomes x diag(d) H / 4; a column block y becomes
 // H diag(d) y / 4, the transpose of the same map.  (Sections 2, 3.4.)
 FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
   // signs and the stride-1 stage together: fl(s_i u_i +- s_j u_j) as one fma of
-  // exact products (the signs are uniform, so s_i costs no vector work)
+  // exact products (the signs are built from bits of the uniform mask, so they
+  // stay scalar operands and s_i costs no vector work)
 #pragma unroll
   for (int i = 0; i < 16; i += 2) {
-    const float si = ((mask >> i) & 1u) ? -1.0f : 1.0f, sj = ((mask >> (i + 1)) & 1u) ? -1.0f : 1.0f;
+    const float si = sign_factor(mask, i), sj = sign_factor(mask, i + 1);
     const float t = sj * u[i + 1];
     const float p = fmaf(si, u[i], t), q = fmaf(si, u[i], -t);
     u[i] = p;
@@ -55,7 +62,7 @@ FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
 FP4R_DEV float rot16_absmax4(float (&u)[16], uint32_t mask) {
 #pragma unroll
   for (int i = 0; i < 16; i += 2) {
-    const float si = ((mask >> i) & 1u) ? -1.0f : 1.0f, sj = ((mask >> (i + 1)) & 1u) ? -1.0f : 1.0f;
+    const float si = sign_factor(mask, i), sj = sign_factor(mask, i + 1);
     const float t = sj * u[i + 1];
     const float p = fmaf(si, u[i], t), q = fmaf(si, u[i], -t);
     u[i] = p;
@@ -161,25 +168,25 @@ struct BlockCand {
 
 // Codes and error sums of a candidate whose scale rs = s s_g is positive, with the
 // E2M1 rounding done by the hardware conversion (round to nearest even, saturating,
-// sign kept) on y = u * r, r ~ 1/rs.  fl32(u / rs) lies strictly between y
-// computed with r (1 - 2^-19) and with r (1 + 2^-19) (r is within 2^-23 of 1/rs,
-// each product within 2^-24), and the rounding is monotone, so when both bracket
-// values give the same codes, fl32(u / rs) gives them too.  Returns false when the
-// codes differ (an element lies next to a grid midpoint) or r is not finite.
+// sign kept) on u * r, r ~ 1/rs.  fl32(u / rs) lies strictly between the products
+// with r (1 - 2^-19) and with r (1 + 2^-19) (r is within 2^-23 of 1/rs, each
+// product within 2^-24), and the rounding is monotone, so when both bracket values
+// give the same codes, fl32(u / rs) gives them too: those are the codes.  Returns
+// false when the codes differ (an element lies next to a grid midpoint) or r is not
+// finite.
 FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
   const float rinv = __builtin_amdgcn_rcpf(rs);
   if (!(rinv < 1e38f)) return false;
   const float rup = rinv * (1.0f + 0x1p-19f), rdn = rinv * (1.0f - 0x1p-19f);
-  uint32_t c[2] = {0u, 0u}, cu[2] = {0u, 0u}, cd[2] = {0u, 0u};
+  uint32_t c[2] = {0u, 0u}, cd[2] = {0u, 0u};
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     const int w = k >> 2;
     const float a = u[2 * k], b = u[2 * k + 1];
     switch (k & 3) {
-#define FP4R_CVT(SEL)                                                                   \
-  case SEL:                                                                             \
-    c[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c[w], a * rinv, b * rinv, 1.0f, SEL); \
-    cu[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(cu[w], a * rup, b * rup, 1.0f, SEL); \
+#define FP4R_CVT(SEL)                                                                  \
+  case SEL:                                                                            \
+    c[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c[w], a * rup, b * rup, 1.0f, SEL);  \
     cd[w] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(cd[w], a * rdn, b * rdn, 1.0f, SEL); \
     break;
       FP4R_CVT(0)
@@ -189,7 +196,7 @@ FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
 #undef FP4R_CVT
     }
   }
-  if (c[0] != cu[0] || c[0] != cd[0] || c[1] != cu[1] || c[1] != cd[1]) return false;
+  if (c[0] != cd[0] || c[1] != cd[1]) return false;
   r.codes = (uint64_t)c[0] | ((uint64_t)c[1] << 32);
   // decoded values q (= tw / 2, signed) back from the codes; u - q rs has the
   // magnitude of |u| - tw (rs / 2), so the sum equals the element-order fma sum
@@ -213,11 +220,24 @@ FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
   return true;
 }
 
+// E4M3 code of min(fl32(bmax / den), 448) for den > 0.  The quotient is taken as
+// bmax * rcp(den), within 4 ulp of fl32(bmax / den) (rcp within 1 ulp of 1/den,
+// one rounding each); the E4M3 rounding only changes at its midpoints, where the
+// 20 bits below the 3-bit mantissa read 0x80000, so a value at least 16 ulp away
+// from one (and in the normal E4M3 range, where the rounding reads those bits)
+// rounds like the quotient itself.  Other values take the correctly rounded
+// division.
+FP4R_DEV uint32_t scale_code(float bmax, float den) {
+  const float rd = __builtin_amdgcn_rcpf(den);
+  const float v = fminf(bmax * rd, 448.0f);
+  const uint32_t rem = __float_as_uint(v) & 0xFFFFFu;
+  if (rd < 1e38f && rd > 1e-37f && v >= 0.015625f && rem - 0x7FFF0u >= 32u) return e4m3_rne(v);
+  return e4m3_rne(fminf(bmax / den, 448.0f));
+}
+
 FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M) {
   BlockCand r;
-  const float den = M * sg;
-  const float v = fminf(bmax / den, 448.0f);
-  r.scale = e4m3_rne(v);
+  r.scale = scale_code(bmax, M * sg);
   const float s = e4m3_value(r.scale);
   const float rs = s * sg;
   r.s = s;

@@ -358,12 +358,21 @@ hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride
 // columns (each of the 16 loads is a contiguous 256-byte wave access).
 
 template <int AXIS>
-FP4R_DEV bool load_block(const Batch& in, int64_t b, int64_t g, float (&u)[16], int64_t& r, int64_t& c) {
-  const float* x = in.x + b * in.bstride;
+FP4R_DEV void block_pos(const Batch& in, int64_t g, int64_t& r, int64_t& c) {
   if (AXIS == 1) {
     const int64_t nbr = in.cols / 16;
     r = g / nbr;
     c = (g % nbr) * 16;
+  } else {
+    c = g % in.cols;
+    r = (g / in.cols) * 16;
+  }
+}
+
+template <int AXIS>
+FP4R_DEV bool load_block_at(const Batch& in, int64_t b, int64_t r, int64_t c, float (&u)[16]) {
+  const float* x = in.x + b * in.bstride;
+  if (AXIS == 1) {
     const float4* p = reinterpret_cast<const float4*>(x + r * in.ld + c);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -371,8 +380,6 @@ FP4R_DEV bool load_block(const Batch& in, int64_t b, int64_t g, float (&u)[16], 
       u[4 * q] = v.x; u[4 * q + 1] = v.y; u[4 * q + 2] = v.z; u[4 * q + 3] = v.w;
     }
   } else {
-    c = g % in.cols;
-    r = (g / in.cols) * 16;
 #pragma unroll
     for (int i = 0; i < 16; ++i) u[i] = x[(r + i) * in.ld + c];
   }
@@ -393,7 +400,8 @@ __global__ __launch_bounds__(256) void k_amax(Batch in, uint32_t mask, int rotat
   if (g < nblk) {
     float u[16];
     int64_t r, c;
-    const bool ok = load_block<AXIS>(in, b, g, u, r, c);
+    block_pos<AXIS>(in, g, r, c);
+    const bool ok = load_block_at<AXIS>(in, b, r, c, u);
     if (!ok) atomicOr(status, kStatusNonFinite);
     if (clip) {
       const float tau = sc[b].tau;
@@ -434,15 +442,21 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   // of a row and the record over the 16 rows reduce within the wave.
   const bool want_rho = AXIS == 1 && out.rhog != nullptr;
   if (g >= nblk) return;   // nblk is a multiple of 64 when records are requested
-  int64_t gb = g;
+  int64_t r, c;
   if (want_rho) {
-    const int64_t nst = in.cols / 64, wv = g >> 6;
-    const int lane = (int)(g & 63);
-    gb = ((wv / nst) * 16 + (lane >> 2)) * (in.cols / 16) + (wv % nst) * 4 + (lane & 3);
+    // the wave index is uniform (waves never straddle a 256-thread group), so the
+    // division by the stage count is scalar work
+    const uint32_t nst = (uint32_t)(in.cols / 64);
+    const uint32_t wv = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 6));
+    const uint32_t rg = wv / nst, st = wv - rg * nst;
+    const int lane = (int)(threadIdx.x & 63);
+    r = (int64_t)rg * 16 + (lane >> 2);
+    c = ((int64_t)st * 4 + (lane & 3)) * 16;
+  } else {
+    block_pos<AXIS>(in, g, r, c);
   }
   float u[16];
-  int64_t r, c;
-  load_block<AXIS>(in, b, gb, u, r, c);
+  load_block_at<AXIS>(in, b, r, c, u);
   if (clip) {
     const float tau = sc[b].tau;
 #pragma unroll
