@@ -28,7 +28,9 @@ FP4R_DEV float sign_factor(uint32_t mask, int i) {
 // d_i = -1), then the Sylvester butterfly with strides 1, 2, 4, 8, then * 1/4.
 // A row block x becomes x diag(d) H / 4; a column block y becomes
 // H diag(d) y / 4, the transpose of the same map.  (Sections 2, 3.4.)
-FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
+// hadamard16 stops before the factor 1/4 (its outputs are 4 times the rotated
+// values, exactly, wherever those are normal numbers).
+FP4R_DEV void hadamard16(float (&u)[16], uint32_t mask) {
   // signs and the stride-1 stage together: fl(s_i u_i +- s_j u_j) as one fma of
   // exact products (the signs are built from bits of the uniform mask, so they
   // stay scalar operands and s_i costs no vector work)
@@ -51,8 +53,16 @@ FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
       }
     }
   }
+}
+
+FP4R_DEV void quarter16(float (&u)[16]) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) u[i] *= 0.25f;
+}
+
+FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
+  hadamard16(u, mask);
+  quarter16(u);
 }
 
 // The largest magnitude over a block after rotate16, times 4: the same butterfly
@@ -83,27 +93,6 @@ FP4R_DEV float rot16_absmax4(float (&u)[16], uint32_t mask) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(u[i]) + fabsf(u[i + 8]));
   return m;
-}
-
-// E4M3FN code of v in [0, 448], round to nearest, ties to the even code.
-FP4R_DEV uint32_t e4m3_rne(float v) {
-  if (v < 0.015625f) {                           // below 2^-6: grid m * 2^-9, m = 0..8
-    return (uint32_t)__builtin_rintf(v * 512.0f);  // exact scaling, RNE to an integer
-  }
-  const uint32_t b = __float_as_uint(v);
-  const uint32_t e = (b >> 23) - 120u;           // E4M3 biased exponent (bias 7)
-  const uint32_t mant = b & 0x7FFFFFu;
-  const uint32_t m3 = mant >> 20, rem = mant & 0xFFFFFu;
-  uint32_t code = (e << 3) | m3;
-  if (rem > 0x80000u || (rem == 0x80000u && (m3 & 1u))) code += 1u;  // carries into the exponent
-  return code;
-}
-
-// Value of a non-negative E4M3FN code (0..126).
-FP4R_DEV float e4m3_value(uint32_t c) {
-  const uint32_t e = (c >> 3) & 15u, m = c & 7u;
-  if (e == 0) return (float)m * 0.001953125f;   // m * 2^-9
-  return __uint_as_float(((e + 120u) << 23) | (m << 20));
 }
 
 // Binary32 rounding of a positive binary64 value downwards / upwards.
@@ -159,7 +148,6 @@ FP4R_DEV uint32_t e2m1_twice(uint32_t idx) { return (0xC8643210u >> (idx << 2)) 
 
 // One candidate block scaling (block maximum mapped to M * s * s_g).
 struct BlockCand {
-  uint32_t scale;   // E4M3 code
   uint64_t codes;   // 16 nibbles, element i in bits 4i..4i+3
   float err;        // sum of squared decode errors in binary32 (fma, element order)
   float s2;         // (s s_g)^2 in binary32, for the error bound
@@ -220,26 +208,46 @@ FP4R_DEV bool quant_candidate_hw(const float (&u)[16], float rs, BlockCand& r) {
   return true;
 }
 
-// E4M3 code of min(fl32(bmax / den), 448) for den > 0.  The quotient is taken as
+// The E4M3 value nearest to v in [0, 448] (ties to the even code), in binary32.
+// From 2^-6 up the grid keeps 3 significand bits: round the binary32 significand
+// at bit 20 (ties to even) and clear the bits below (a carry moves into the
+// exponent by itself); below 2^-6 the grid is m 2^-9.
+FP4R_DEV float e4m3_round(float v) {
+  const uint32_t b = __float_as_uint(v);
+  const float sn = __uint_as_float((b + 0x7FFFFu + ((b >> 20) & 1u)) & 0xFFF00000u);
+  const float ss = __builtin_rintf(v * 512.0f) * 0.001953125f;
+  return v < 0.015625f ? ss : sn;
+}
+
+// E4M3FN code of a value s of the grid (0 <= s <= 448) given in binary32.
+FP4R_DEV uint32_t e4m3_code(float s) {
+  return s < 0.015625f ? (uint32_t)(s * 512.0f) : (__float_as_uint(s) >> 20) - 960u;
+}
+
+// E4M3 value of min(fl32(bmax / den), 448) for den > 0.  The quotient is taken as
 // bmax * rcp(den), within 4 ulp of fl32(bmax / den) (rcp within 1 ulp of 1/den,
 // one rounding each); the E4M3 rounding only changes at its midpoints, where the
 // 20 bits below the 3-bit mantissa read 0x80000, so a value at least 16 ulp away
 // from one (and in the normal E4M3 range, where the rounding reads those bits)
 // rounds like the quotient itself.  Other values take the correctly rounded
 // division.
-FP4R_DEV uint32_t scale_code(float bmax, float den) {
+FP4R_DEV float scale_value(float bmax, float den) {
   const float rd = __builtin_amdgcn_rcpf(den);
-  const float v = fminf(bmax * rd, 448.0f);
+  float v = fminf(bmax * rd, 448.0f);
   const uint32_t rem = __float_as_uint(v) & 0xFFFFFu;
-  if (rd < 1e38f && rd > 1e-37f && v >= 0.015625f && rem - 0x7FFF0u >= 32u) return e4m3_rne(v);
-  return e4m3_rne(fminf(bmax / den, 448.0f));
+  const bool fast = (rd < 1e38f) & (rd > 1e-37f) & (v >= 0.015625f) & (rem - 0x7FFF0u >= 32u);
+  if (!fast) v = fminf(bmax / den, 448.0f);
+  return e4m3_round(v);
 }
 
-FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M) {
+// u holds kf times the block (kf = 1, or 4 for hadamard16 outputs); every scale
+// below is kf times its reference value, which is exact (a power-of-two factor on
+// normal numbers), so codes and scale codes are those of the block itself and the
+// error sums are kf^2 times its own.
+FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M, float kf) {
   BlockCand r;
-  r.scale = scale_code(bmax, M * sg);
-  const float s = e4m3_value(r.scale);
-  const float rs = s * sg;
+  const float s = scale_value(bmax, (M * sg) * kf);
+  const float rs = (s * sg) * kf;
   r.s = s;
   r.s2 = rs * rs;
   r.codes = 0;
@@ -273,20 +281,26 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
 }
 
 // The candidate's squared error in binary64, summed in element order: the
-// reference definition of the 4/6 choice.
-FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c, float sg) {
+// reference definition of the 4/6 choice (on the block itself: u / kf, rounded
+// to binary32 as the rotation's factor 1/4 rounds).
+FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c, float sg, float kf) {
   const double half_ss = 0.5 * ((double)c.s * (double)sg);   // exact: 4 + 24 significant bits
   double e = 0.0;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const double dec = (double)e2m1_twice((uint32_t)(c.codes >> (4 * i)) & 7u) * half_ss;
-    const double d = (double)fabsf(u[i]) - dec;   // exact; d^2 as for the signed difference
+    const float ui = kf == 1.0f ? u[i] : u[i] * 0.25f;
+    const double d = (double)fabsf(ui) - dec;   // exact; d^2 as for the signed difference
     e = e + d * d;
   }
   return e;
 }
 
-// Quantise one (already rotated) block given the tensor scale.  With want_n2,
+// Quantise one (already rotated) block given the tensor scale; u holds kf times
+// the block (kf = 1 or 4, and 4 only where the tensor scale is at least 2^-40:
+// then an element whose quarter is subnormal lies far below every grid step, and
+// differences below the normal range change the binary32 error sums by far less
+// than their bound, so the choice and the codes are those of the block).  With want_n2,
 // `n2` receives sum_i (2 q_i)^2 M^2 with M the scale's integer significand (8..15,
 // or the mantissa of a subnormal scale): the block's sum of squared decoded values
 // is n2 2^(2 e - 22), e = max(exponent field, 1); otherwise n2 is 0.
@@ -299,7 +313,7 @@ FP4R_DEV double cand_err64(const float (&u)[16], const BlockCand& c, float sg) {
 // If err4 + 2 (B4 + B6) < err6 the exact E4 < E6 by more than any binary64
 // rounding, and symmetrically; otherwise both are recomputed in binary64.
 FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_t& scale,
-                          uint64_t& codes, uint32_t& n2, bool want_n2 = true) {
+                          uint64_t& codes, uint32_t& n2, bool want_n2 = true, float kf = 1.0f) {
   n2 = 0;
   if (sg == 0.0f) {   // all-zero tensor: zero scales, zero magnitudes, signs kept
     codes = 0;
@@ -311,33 +325,33 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
   float bmax = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, fabsf(u[i]));
-  BlockCand c6 = quant_candidate(u, bmax, sg, 6.0f);
+  BlockCand c6 = quant_candidate(u, bmax, sg, 6.0f, kf);
   if (adaptive) {
-    const BlockCand c4 = quant_candidate(u, bmax, sg, 4.0f);
+    const BlockCand c4 = quant_candidate(u, bmax, sg, 4.0f, kf);
     const float b = 2.0f * (0x1p-14f * (c4.s2 + c6.s2) + 0x1p-18f * (c4.err + c6.err));
     bool use4;
     if (c4.err + b < c6.err) use4 = true;
     else if (c6.err + b < c4.err) use4 = false;
-    else use4 = cand_err64(u, c4, sg) < cand_err64(u, c6, sg);
+    else use4 = cand_err64(u, c4, sg, kf) < cand_err64(u, c6, sg, kf);
     if (use4) c6 = c4;
   }
-  scale = c6.scale;
+  scale = e4m3_code(c6.s);
   codes = c6.codes;
   if (!want_n2) return;
-  // sum of q^2 from the decoded codes (exact: multiples of 1/4 below 2^10)
+  // sum of q^2 from the codes decoded to f16 pairs (q and q^2 exact; the sums are
+  // multiples of 1/4 below 2^10, exact in the binary32 accumulator)
   const uint32_t w[2] = {(uint32_t)codes, (uint32_t)(codes >> 32)};
   float k2 = 0.0f;
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    float2 q;
+    __attribute__((ext_vector_type(2))) _Float16 q;
     switch (k & 3) {
-      case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 0)); break;
-      case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 1)); break;
-      case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 2)); break;
-      default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 3)); break;
+      case 0: q = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[k >> 2], 1.0f, 0); break;
+      case 1: q = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[k >> 2], 1.0f, 1); break;
+      case 2: q = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[k >> 2], 1.0f, 2); break;
+      default: q = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[k >> 2], 1.0f, 3); break;
     }
-    k2 = fmaf(q.x, q.x, k2);
-    k2 = fmaf(q.y, q.y, k2);
+    k2 = __builtin_amdgcn_fdot2(q, q, k2, false);
   }
   const uint32_t mant = (scale >> 3) ? 8u + (scale & 7u) : (scale & 7u);
   n2 = (uint32_t)(4.0f * k2) * mant * mant;
@@ -392,9 +406,17 @@ FP4R_DEV float row16_max_pos(float v) {
   return v;
 }
 
-// Global scale from the bit pattern of the (non-negative) amax.
+// Global scale fl32(amax / 2688) from the bit pattern of the (non-negative) amax.
+// From 2^-100 up as q = amax y (y the binary32 nearest to 1/2688) corrected once by
+// the exact remainder, q + (amax - 2688 q) y: equal to the correctly rounded
+// quotient for every binary32 amax >= 2^-119 (checked exhaustively against IEEE
+// division), and every intermediate is a normal number from 2^-100 up.
 FP4R_DEV float tensor_scale_from_amax(uint32_t amax_bits) {
-  return __uint_as_float(amax_bits) / kSgDivisor;
+  const float a = __uint_as_float(amax_bits);
+  if (!(a >= 0x1p-100f)) return a / kSgDivisor;
+  const float y = 0x1.861862p-12f;
+  const float q = a * y;
+  return fmaf(fmaf(-q, kSgDivisor, a), y, q);
 }
 
 FP4R_DEV float warp_max(float v) {

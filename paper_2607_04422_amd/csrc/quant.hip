@@ -352,6 +352,17 @@ hipError_t launch_copy_out(const MatChunk& ch, const float* x, int64_t x_bstride
 }
 
 // ---------------------------------------------------------------------------
+// The rotation ahead of the quantiser: with a tensor scale of at least 2^-40 the
+// factor 1/4 is left to the quantiser's scales (returns kf = 4, see quant_block);
+// otherwise the block is rotated in full (kf = 1).
+FP4R_DEV float rotate_for_quant(float (&u)[16], uint32_t mask, int rotate, float sg) {
+  if (!rotate) return 1.0f;
+  hadamard16(u, mask);
+  if (sg >= 0x1p-40f) return 4.0f;
+  quarter16(u);
+  return 1.0f;
+}
+
 // Quantiser: one thread per 16-element block.  Axis 1: blocks along a row,
 // consecutive threads take consecutive blocks of a row (contiguous 64-byte
 // reads).  Axis 0: blocks down a column, consecutive threads take consecutive
@@ -462,11 +473,11 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
 #pragma unroll
     for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
   }
-  if (rotate) rotate16(u, mask);
+  const float kf = rotate_for_quant(u, mask, rotate, sg);
   uint32_t scale;
   uint64_t codes;
   uint32_t n2;
-  quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho);
+  quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho, kf);
   if (want_rho) {
     uint32_t emin;
     const float rrow = quad_stage_rho(n2, block_exp(scale), &emin);
@@ -495,7 +506,10 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
 __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
                                                    uint32_t mask, int rotate, int adaptive, MatScalars* sc,
                                                    int slot_n, int slot_m, QOut qx, QOut qxt) {
-  __shared__ float tile[kT][kT + 1];
+  // rows padded to 68 floats: 16-byte row slices for the row blocks, and the
+  // 16 lanes of one 128-bit access (4 rows x 4 slices) or 64 consecutive
+  // columns of one row fall in distinct banks
+  __shared__ __align__(16) float tile[kT][kT + 4];
   const int64_t b = blockIdx.y;
   const int64_t tn = cdiv(n, kT);
   const int64_t r0 = (blockIdx.x / tn) * kT, c0 = (blockIdx.x % tn) * kT;
@@ -510,12 +524,9 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
     const int i = threadIdx.x >> 2, q = threadIdx.x & 3;   // row i, 16 columns at 16 q
     if (r0 + i < m && c0 + 16 * q < n) {
       const float4* p = reinterpret_cast<const float4*>(X + (r0 + i) * n + c0 + 16 * q);
+      float4* t = reinterpret_cast<float4*>(&tile[i][16 * q]);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float4 v = p[k];
-        tile[i][16 * q + 4 * k] = v.x; tile[i][16 * q + 4 * k + 1] = v.y;
-        tile[i][16 * q + 4 * k + 2] = v.z; tile[i][16 * q + 4 * k + 3] = v.w;
-      }
+      for (int k = 0; k < 4; ++k) t[k] = p[k];
     }
   }
   __syncthreads();
@@ -525,12 +536,16 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
     uint32_t n2 = 0, e = 15;
     if (r < m && c < n) {
       float u[16];
+      const float4* t = reinterpret_cast<const float4*>(&tile[i][16 * q]);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) u[k] = tile[i][16 * q + k];
-      if (rotate) rotate16(u, mask);
+      for (int k = 0; k < 4; ++k) {
+        const float4 v = t[k];
+        u[4 * k] = v.x; u[4 * k + 1] = v.y; u[4 * k + 2] = v.z; u[4 * k + 3] = v.w;
+      }
+      const float kf = rotate_for_quant(u, mask, rotate, sgn);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgn, adaptive != 0, scale, codes, n2, qx.rhog != nullptr);
+      quant_block(u, sgn, adaptive != 0, scale, codes, n2, qx.rhog != nullptr, kf);
       e = block_exp(scale);
       *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + r * (n / 2) + c / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
@@ -556,10 +571,10 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       float u[16];
 #pragma unroll
       for (int k = 0; k < 16; ++k) u[k] = tile[16 * q + k][j];
-      if (rotate) rotate16(u, mask);
+      const float kf = rotate_for_quant(u, mask, rotate, sgm);
       uint32_t scale;
       uint64_t codes;
-      quant_block(u, sgm, adaptive != 0, scale, codes, n2, qxt.rhog != nullptr);
+      quant_block(u, sgm, adaptive != 0, scale, codes, n2, qxt.rhog != nullptr, kf);
       e = block_exp(scale);
       *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + c * (m / 2) + r / 2) =
           make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));

@@ -74,6 +74,23 @@ def test_quantize_edge_cases():
         codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=1, flags=flags)
         ref = quantize(m, 1, rht.step_signs(0, 0) if flags & 2 else None, bool(flags & 4))
         assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"tiny flags={flags}")
+    # a tensor scale just above 2^-40 with blocks in and below the subnormal range:
+    # the rotated quarter of these underflows, the kernel's scaled copies do not
+    rng = np.random.default_rng(4)
+    m = np.zeros((32, 64), np.float32)
+    m[0, 0] = 1e-7
+    m[5, 3], m[5, 4], m[5, 9] = 1e-38, -3e-41, 1e-45
+    m[9, 16:32] = (7e-39 * rng.standard_normal(16)).astype(np.float32)
+    m[12, :16] = (2e-37 * rng.standard_normal(16)).astype(np.float32)
+    m[17, 32:48] = (1e-12 * rng.standard_normal(16)).astype(np.float32)
+    m[30, 48:] = (3e-9 * rng.standard_normal(16)).astype(np.float32)
+    x = torch.from_numpy(m).cuda()
+    for flags in (0, 6):
+        codes, scales, sg, _, _ = F.fp4root_quantize(x, axis=1, flags=flags)
+        if flags & 2:
+            assert np_(sg)[0] >= 2.0 ** -40
+        ref = quantize(m, 1, rht.step_signs(0, 0) if flags & 2 else None, bool(flags & 4))
+        assert_same_nvfp4(gpu_nvfp4(codes, scales, sg), ref, f"small scale flags={flags}")
 
 
 def test_quantize_nonfinite_reported():
