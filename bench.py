@@ -47,15 +47,35 @@ def set_flop(shapes, steps):
     return sum(ns_flop(min(r, c), max(r, c), steps) for (r, c) in shapes)
 
 
-def time_calls(fn, warmup, iters, torch):
+def time_calls(fn, warmup, iters, torch, per_call=None):
+    """Mean wall time of `iters` calls after `warmup` (synchronised on both sides).
+    With a list `per_call`, also appends each call's duration in ms from HIP events
+    recorded between the calls on the launch stream (torch's current stream)."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)] if per_call is not None else None
     t0 = time.perf_counter()
-    for _ in range(iters):
+    for i in range(iters):
+        if evs:
+            evs[i].record()
         fn()
+    if evs:
+        evs[iters].record()
     torch.cuda.synchronize()
-    return (time.perf_counter() - t0) / iters
+    t = (time.perf_counter() - t0) / iters
+    if evs:
+        per_call.extend(evs[i].elapsed_time(evs[i + 1]) for i in range(iters))
+    return t
+
+
+def spread(ms):
+    """Median and 10th / 90th percentiles of per-call times (ms)."""
+    v = sorted(ms)
+    if not v:
+        return None
+    q = lambda f: v[min(len(v) - 1, max(0, int(round(f * (len(v) - 1)))))]
+    return {"median": round(q(0.5), 3), "p10": round(q(0.1), 3), "p90": round(q(0.9), 3), "calls": len(v)}
 
 
 def torch_bf16_reference(inputs, coeffs_for, steps, warmup, iters, torch):
@@ -175,7 +195,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"probe": args.case, "copy_bytes": COPY_PROBE_BYTES}), flush=True)
         return
-    t_step = time_calls(orth, args.warmup, args.steps, torch)
+    calls = []
+    t_step = time_calls(orth, args.warmup, args.steps, torch, calls)
     value = len(shapes) / t_step
     tflops = flop / t_step / 1e12
 
@@ -213,8 +234,10 @@ def main():
     if not args.no_bf16:
         orth16 = F.Orthogonalizer(inputs, steps=S, flags=F.F_CLIP | F.F_BF16_PATH, clip_quantile=0.99,
                                   eps=1e-7, seed=0)
-        t16 = time_calls(orth16, args.warmup, args.steps, torch)
-        bf16 = {"ms_per_step": round(t16 * 1e3, 3), "matrices_per_s": round(len(shapes) / t16, 2),
+        calls16 = []
+        t16 = time_calls(orth16, args.warmup, args.steps, torch, calls16)
+        bf16 = {"ms_per_step": round(t16 * 1e3, 3), "per_call_ms": spread(calls16),
+                "matrices_per_s": round(len(shapes) / t16, 2),
                 "tflops_effective": round(flop / t16 / 1e12, 2),
                 "pct_bf16_peak": round(100 * flop / t16 / 1e12 / BF16_MFMA_PEAK_TFLOPS, 2),
                 "nvfp4_speedup_vs_bf16": round(t16 / t_step, 3)}
@@ -235,6 +258,7 @@ def main():
     line = {
         "metric": METRIC, "value": round(value, 3), "unit": "matrices/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_step * 1e3, 3),
+        "per_call_ms": spread(calls),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "nvfp4 operands; f16 MFMA exact block products; f64 accumulation",
         "data": "synthetic",
