@@ -77,8 +77,11 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t n, hipStream_t s
 
 // Quantile of |x| per matrix in the chunk; writes sc[i].tau (ranks lo, lo+1).
 // hist: chunk.count * 2 * kHistBins words of scratch.  status: device word.
+// With psum / pcnt (chunk.total_tiles doubles / words of scratch) it also writes
+// sc[i].inv_norm = fl32(1/(||clamp(M, tau)|| + eps)), as launch_inv_norm does.
 hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* hist,
-                                 uint32_t* status, hipStream_t st);
+                                 uint32_t* status, hipStream_t st, double* psum = nullptr,
+                                 uint32_t* pcnt = nullptr, float eps = 0.0f);
 
 // Frobenius norm of the clipped matrices: sc[i].inv_norm = fl32(1/(||.|| + eps)).
 // partial: chunk.total_tiles doubles of scratch.

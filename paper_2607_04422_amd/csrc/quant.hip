@@ -33,6 +33,14 @@ FP4R_DEV int find_matrix(const MatChunk& ch, int64_t tile) {
 // Clip threshold: tau = fl32(v[lo] + f (v[lo+1] - v[lo])) over the sorted |M|,
 // found with a three-pass radix select on the binary32 bit patterns (31-bit keys,
 // digits of 11, 10 and 10 bits).  Both ranks are tracked in the same passes.
+//
+// The last pass can also give the Frobenius norm of clamp(M, tau): by then the
+// 21-bit key prefixes p0 <= p1 of v[lo] and v[lo+1] are known, tau lies between
+// the two, and no element lies strictly between them, so an element whose prefix
+// is below p0 is not clipped (its square goes into a binary64 partial of the
+// block), one above p1 is clipped to tau (it is only counted), and the elements
+// with prefix p0 or p1 are exactly the pass's histograms (a key is the bit
+// pattern of |x|), which the select step sums in bin order once tau is known.
 
 __global__ void k_clip_init(MatChunk ch, MatScalars* sc) {
   const int i = threadIdx.x;
@@ -46,8 +54,11 @@ __global__ void k_clip_init(MatChunk ch, MatScalars* sc) {
 }
 
 __global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalars* sc,
-                                                    uint32_t* hist, uint32_t* status, int pass) {
+                                                    uint32_t* hist, uint32_t* status, int pass,
+                                                    double* psum, uint32_t* pcnt) {
   __shared__ uint32_t h[2][kHistBins];
+  __shared__ double red[256];
+  __shared__ uint32_t above_all;
   for (int i = threadIdx.x; i < 2 * kHistBins; i += 256) (&h[0][0])[i] = 0;
   __syncthreads();
   const int64_t tile = blockIdx.x;
@@ -58,6 +69,10 @@ __global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalar
   const uint32_t p0 = sc[mi].sel_prefix[0], p1 = sc[mi].sel_prefix[1];
   const bool two = pass > 0 && p0 != p1;
   const int pshift = pass == 1 ? 20 : 10;
+  const bool norm = pass == 2 && psum != nullptr;
+  double acc = 0.0;     // squares of the elements below prefix p0, in this thread's order
+  uint32_t above = 0;   // elements above prefix p1
+  if (threadIdx.x == 0) above_all = 0;
   bool bad = false;
   for (int64_t r = r0; r < r1; ++r) {
     const float4* row = reinterpret_cast<const float4*>(d.in + r * d.ld_in);
@@ -77,11 +92,33 @@ __global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalar
         const uint32_t pre = key >> pshift;
         if (pre == p0) atomicAdd(&h[0][digit], 1u);
         if (two && pre == p1) atomicAdd(&h[1][digit], 1u);
+        if (norm) {
+          if (pre < p0) {
+            const double x = (double)e[j];
+            acc = acc + x * x;
+          } else if (pre > p1) {
+            ++above;
+          }
+        }
       }
     }
   }
   if (bad) atomicOr(status, kStatusNonFinite);
+  if (norm) {
+    red[threadIdx.x] = acc;
+    if (above) atomicAdd(&above_all, above);
+  }
   __syncthreads();
+  if (norm) {
+    for (int off = 128; off > 0; off >>= 1) {   // fixed-order tree
+      if ((int)threadIdx.x < off) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + off];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      psum[tile] = red[0];
+      pcnt[tile] = above_all;
+    }
+  }
   const int nb = pass == 0 ? 2048 : 1024;
   for (int b = threadIdx.x; b < nb; b += 256) {
     if (h[0][b]) atomicAdd(&hist[(mi * 2 + 0) * kHistBins + b], h[0][b]);
@@ -90,9 +127,12 @@ __global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalar
 }
 
 __global__ __launch_bounds__(256) void k_radix_select(MatChunk ch, MatScalars* sc, uint32_t* hist,
-                                                      int pass) {
+                                                      int pass, const double* psum, const uint32_t* pcnt,
+                                                      float eps) {
   __shared__ uint32_t part[256];
   __shared__ uint32_t found_prefix[2], found_rank[2];
+  __shared__ double red[256];
+  __shared__ unsigned long long above_all;
   const int mi = blockIdx.x;
   const int t = threadIdx.x;
   MatScalars& s = sc[mi];
@@ -129,6 +169,57 @@ __global__ __launch_bounds__(256) void k_radix_select(MatChunk ch, MatScalars* s
     }
     __syncthreads();
   }
+  if (pass == 2 && psum) {
+    // ||clamp(M, tau)||^2 in a fixed order: the blocks' partials below p0, the
+    // elements of the two prefixes from the histograms (bin order), the elements
+    // above p1 at tau^2 each
+    const MatDesc& d = ch.m[mi];
+    const double v0 = (double)__uint_as_float(found_prefix[0]);
+    const double v1 = (double)__uint_as_float(found_prefix[1]);
+    const float tau = (float)__dadd_rn(v0, __dmul_rn(d.frac, __dsub_rn(v1, v0)));
+    if (t == 0) above_all = 0;
+    const int64_t nt = (d.rows + kPrepRowsPerBlock - 1) / kPrepRowsPerBlock;
+    double below = 0.0;
+    unsigned long long above = 0;
+    for (int64_t i = t; i < nt; i += 256) {
+      below = below + psum[d.tile_begin + i];
+      above += pcnt[d.tile_begin + i];
+    }
+    double cand = 0.0;
+    for (int rr = 0; rr < (two ? 2 : 1); ++rr) {
+      const uint32_t* hh = hist + (mi * 2 + rr) * kHistBins;
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t bin = (uint32_t)(4 * t + j), c = hh[bin];
+        if (c) {
+          const double x = (double)fminf(__uint_as_float((s.sel_prefix[rr] << 10) | bin), tau);
+          cand = cand + (double)c * (x * x);
+        }
+      }
+    }
+    __syncthreads();
+    atomicAdd(&above_all, above);
+    red[t] = below;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+      if (t < off) red[t] = red[t] + red[t + off];
+      __syncthreads();
+    }
+    const double sum_below = red[0];
+    __syncthreads();
+    red[t] = cand;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+      if (t < off) red[t] = red[t] + red[t + off];
+      __syncthreads();
+    }
+    if (t == 0) {
+      const double tt = (double)tau * (double)tau;
+      const double total = __dadd_rn(__dadd_rn(sum_below, red[0]), __dmul_rn((double)above_all, tt));
+      const double nu = __dsqrt_rn(total);
+      s.inv_norm = (float)__ddiv_rn(1.0, __dadd_rn(nu, (double)eps));
+    }
+    __syncthreads();
+  }
   for (int b = t; b < 2 * kHistBins; b += 256) hist[mi * 2 * kHistBins + b] = 0u;
   if (t == 0) {
     s.sel_prefix[0] = found_prefix[0];
@@ -145,14 +236,16 @@ __global__ __launch_bounds__(256) void k_radix_select(MatChunk ch, MatScalars* s
 }
 
 hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* hist,
-                                 uint32_t* status, hipStream_t st) {
+                                 uint32_t* status, hipStream_t st, double* psum, uint32_t* pcnt,
+                                 float eps) {
   hipError_t e = launch_fill_u32(hist, 0u, (int64_t)ch.count * 2 * kHistBins, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_clip_init, dim3(1), dim3(kMaxChunk), 0, st, ch, sc);
   for (int pass = 0; pass < 3; ++pass) {
     hipLaunchKernelGGL(k_radix_hist, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc,
-                       hist, status, pass);
-    hipLaunchKernelGGL(k_radix_select, dim3(ch.count), dim3(256), 0, st, ch, sc, hist, pass);
+                       hist, status, pass, psum, pcnt);
+    hipLaunchKernelGGL(k_radix_select, dim3(ch.count), dim3(256), 0, st, ch, sc, hist, pass,
+                       (const double*)psum, (const uint32_t*)pcnt, eps);
   }
   return hipGetLastError();
 }
