@@ -353,8 +353,9 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
     }
     k2 = __builtin_amdgcn_fdot2(q, q, k2, false);
   }
-  const uint32_t mant = (scale >> 3) ? 8u + (scale & 7u) : (scale & 7u);
-  n2 = (uint32_t)(4.0f * k2) * mant * mant;
+  // n2 = 4 k2 M^2 < 2^24: exact in binary32
+  const float mant = (float)((scale >> 3) ? 8u + (scale & 7u) : (scale & 7u));
+  n2 = (uint32_t)((4.0f * k2) * (mant * mant));
 }
 
 // Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a
@@ -372,16 +373,20 @@ FP4R_DEV float stage_rho(const uint32_t (&n2)[4], const uint32_t (&e)[4]) {
   return ru32(r);   // the sum is exact in binary64 (terms n2 < 2^19 times 4^k, k <= 14)
 }
 
+// Lane moves within a row of 16 lanes (DPP; every source lane of the patterns used
+// exists, and all lanes of the wave must be active): quad_perm broadcasts of lane k
+// of each quad (0x00, 0x55, 0xAA, 0xFF), xor 1 (0xB1), xor 2 (0x4E), mirror within
+// 8 lanes (0x141) and within 16 lanes (0x140).
+template <int CTRL>
+FP4R_DEV uint32_t dpp_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+
 // The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3, and
-// (optionally) the row's e_min over the stage.
+// (optionally) the row's e_min over the stage.  All lanes of the wave must be active.
 FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e, uint32_t* emin = nullptr) {
-  uint32_t qn[4], qe[4];
-  const int base = (int)(threadIdx.x & 60u);
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    qn[k] = (uint32_t)__shfl((int)n2, base + k, 64);
-    qe[k] = (uint32_t)__shfl((int)e, base + k, 64);
-  }
+  const uint32_t qn[4] = {dpp_u<0x00>(n2), dpp_u<0x55>(n2), dpp_u<0xAA>(n2), dpp_u<0xFF>(n2)};
+  const uint32_t qe[4] = {dpp_u<0x00>(e), dpp_u<0x55>(e), dpp_u<0xAA>(e), dpp_u<0xFF>(e)};
   if (emin) *emin = min(min(qe[0], qe[1]), min(qe[2], qe[3]));
   return stage_rho(qn, qe);
 }
@@ -394,16 +399,21 @@ FP4R_DEV float pair_rho(float r0, uint32_t e0, float r1, uint32_t e1) {
   return ru32(ldexp((double)r0, 2 * (int)(e0 - e)) + ldexp((double)r1, 2 * (int)(e1 - e)));
 }
 
-// Maximum of non-negative values over the wave / over each 16 lanes.
-FP4R_DEV float wave_max_pos(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+// Maximum of non-negative values over each 16 lanes / over the wave (compared as
+// bit patterns, which order non-negative floats); all lanes of the wave must be
+// active, and every lane gets the result.
+FP4R_DEV uint32_t row16_max_bits(uint32_t b) {
+  b = max(b, dpp_u<0xB1>(b));
+  b = max(b, dpp_u<0x4E>(b));
+  b = max(b, dpp_u<0x141>(b));
+  return max(b, dpp_u<0x140>(b));
 }
-FP4R_DEV float row16_max_pos(float v) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+FP4R_DEV float row16_max_pos(float v) { return __uint_as_float(row16_max_bits(__float_as_uint(v))); }
+FP4R_DEV float wave_max_pos(float v) {
+  const uint32_t b = row16_max_bits(__float_as_uint(v));
+  const uint32_t r0 = __builtin_amdgcn_readlane(b, 0), r1 = __builtin_amdgcn_readlane(b, 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(b, 32), r3 = __builtin_amdgcn_readlane(b, 48);
+  return __uint_as_float(max(max(r0, r1), max(r2, r3)));
 }
 
 // Global scale fl32(amax / 2688) from the bit pattern of the (non-negative) amax.

@@ -604,8 +604,8 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
   // columns of one row fall in distinct banks
   __shared__ __align__(16) float tile[kT][kT + 4];
   const int64_t b = blockIdx.y;
-  const int64_t tn = cdiv(n, kT);
-  const int64_t r0 = (blockIdx.x / tn) * kT, c0 = (blockIdx.x % tn) * kT;
+  const uint32_t tn = (uint32_t)cdiv(n, kT);   // tiles per row of tiles (grid.x < 2^32)
+  const int64_t r0 = (int64_t)(blockIdx.x / tn) * kT, c0 = (int64_t)(blockIdx.x % tn) * kT;
   const float* X = x + b * x_bstride;
   const float sgn = tensor_scale_from_amax(amax_read(sc[b], slot_n));
   const float sgm = tensor_scale_from_amax(amax_read(sc[b], slot_m));
