@@ -118,6 +118,11 @@ struct QOut {
   // of the row}, [K/64][rows], the input of the two-stage records below
   uint2* rowst = nullptr;
   int64_t rowst_bstride = 0;
+  // optional, with rhog, single-axis encoder only (K a multiple of 128): the
+  // two-stage records themselves, [K/128][rows/16] (as launch_pair_records
+  // writes them from rowst)
+  float* rho8 = nullptr;
+  int64_t rho8_bstride = 0;
 };
 
 // Two-stage chain records from the per-row stage data: for stage pairs (2p, 2p+1)
@@ -139,9 +144,12 @@ hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rot
 
 // Both quantisations of X (m x n, row stride n) from one read: qX along n into
 // qx (slot_n), qXt along m into qxt (slot_m, stored transposed).
+// reset_mask: amax slots of every matrix set to zero by the launch (for the
+// products that run after it; never slot_n or slot_m), as launch_reset_scalars does.
 hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
                             uint32_t sign_mask, bool rotate, bool adaptive46, MatScalars* sc,
-                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st);
+                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st,
+                            uint32_t reset_mask = 0);
 
 // ---------------------------------------------------------------------------
 // GEMMs (all operands K-contiguous: C[i][j] = sum_k A[i][k] B[j][k]).

@@ -543,54 +543,75 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   }
   // With chain records (axis 1, cols a multiple of 64) each wave takes 16 rows x
   // one 64-column stage: lane 4i + k holds block k of row i, so the stage bound
-  // of a row and the record over the 16 rows reduce within the wave.
+  // of a row and the record over the 16 rows reduce within the wave.  With
+  // two-stage records (cols a multiple of 128) waves 2p and 2p + 1 of a group
+  // hold stages 2s and 2s + 1 of the same rows, and exchange their row records.
   const bool want_rho = AXIS == 1 && out.rhog != nullptr;
-  if (g >= nblk) return;   // nblk is a multiple of 64 when records are requested
-  int64_t r, c;
+  const bool pairs = want_rho && out.rho8 != nullptr;
+  if (g >= nblk && !pairs) return;   // nblk is a multiple of 64 when records are requested
+  const bool live = g < nblk;        // uniform over a wave when records are requested
+  int64_t r = 0, c = 0;
+  uint32_t rg = 0, st = 0;
   if (want_rho) {
     // the wave index is uniform (waves never straddle a 256-thread group), so the
     // division by the stage count is scalar work
     const uint32_t nst = (uint32_t)(in.cols / 64);
     const uint32_t wv = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 6));
-    const uint32_t rg = wv / nst, st = wv - rg * nst;
+    rg = wv / nst;
+    st = wv - rg * nst;
     const int lane = (int)(threadIdx.x & 63);
     r = (int64_t)rg * 16 + (lane >> 2);
     c = ((int64_t)st * 4 + (lane & 3)) * 16;
   } else {
     block_pos<AXIS>(in, g, r, c);
   }
-  float u[16];
-  load_block_at<AXIS>(in, b, r, c, u);
-  if (clip) {
-    const float tau = sc[b].tau;
+  float rrow = 0.0f;
+  uint32_t emin = 15;
+  if (live) {
+    float u[16];
+    load_block_at<AXIS>(in, b, r, c, u);
+    if (clip) {
+      const float tau = sc[b].tau;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
+      for (int i = 0; i < 16; ++i) u[i] = fminf(fmaxf(u[i], -tau), tau);
+    }
+    const float kf = rotate_for_quant(u, mask, rotate, sg);
+    uint32_t scale;
+    uint64_t codes;
+    uint32_t n2;
+    quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho, kf);
+    if (want_rho) {
+      rrow = quad_stage_rho(n2, block_exp(scale), &emin);
+      if (out.rowst && (threadIdx.x & 3) == 0)
+        out.rowst[b * out.rowst_bstride + (c / 64) * in.rows + r] = make_uint2(__float_as_uint(rrow), emin);
+      const float rho = wave_max_pos(rrow);
+      if ((threadIdx.x & 63) == 0)
+        out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
+    }
+    int64_t code_off, scale_off;
+    if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
+      code_off = r * (in.cols / 2) + c / 2;
+      scale_off = r * (in.cols / 16) + c / 16;
+    } else {           // transposed: [cols][rows/2], [cols][rows/16]
+      code_off = c * (in.rows / 2) + r / 2;
+      scale_off = c * (in.rows / 16) + r / 16;
+    }
+    *reinterpret_cast<uint2*>(out.codes + b * out.codes_bstride + code_off) =
+        make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+    out.scales[b * out.scales_bstride + scale_off] = (uint8_t)scale;
   }
-  const float kf = rotate_for_quant(u, mask, rotate, sg);
-  uint32_t scale;
-  uint64_t codes;
-  uint32_t n2;
-  quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho, kf);
-  if (want_rho) {
-    uint32_t emin;
-    const float rrow = quad_stage_rho(n2, block_exp(scale), &emin);
-    if (out.rowst && (threadIdx.x & 3) == 0)
-      out.rowst[b * out.rowst_bstride + (c / 64) * in.rows + r] = make_uint2(__float_as_uint(rrow), emin);
-    const float rho = wave_max_pos(rrow);
-    if ((threadIdx.x & 63) == 0)
-      out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
+  if (pairs) {
+    // every wave of the group reaches the barrier (none has returned)
+    __shared__ uint2 odd_rows[2][16];
+    const int w = (int)(threadIdx.x >> 6), i = (int)((threadIdx.x & 63) >> 2);
+    if (live && (w & 1) && (threadIdx.x & 3) == 0) odd_rows[w >> 1][i] = make_uint2(__float_as_uint(rrow), emin);
+    __syncthreads();
+    if (live && !(w & 1)) {
+      const uint2 o = odd_rows[w >> 1][i];
+      const float r8 = wave_max_pos(pair_rho(rrow, emin, __uint_as_float(o.x), o.y));
+      if ((threadIdx.x & 63) == 0) out.rho8[b * out.rho8_bstride + (st / 2) * (in.rows / 16) + rg] = r8;
+    }
   }
-  int64_t code_off, scale_off;
-  if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
-    code_off = r * (in.cols / 2) + c / 2;
-    scale_off = r * (in.cols / 16) + c / 16;
-  } else {           // transposed: [cols][rows/2], [cols][rows/16]
-    code_off = c * (in.rows / 2) + r / 2;
-    scale_off = c * (in.rows / 16) + r / 16;
-  }
-  *reinterpret_cast<uint2*>(out.codes + b * out.codes_bstride + code_off) =
-      make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
-  out.scales[b * out.scales_bstride + scale_off] = (uint8_t)scale;
 }
 
 // Both quantisations of X from one read: a 64 x 64 tile is staged in LDS; each
@@ -598,7 +619,7 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
 // along m, written transposed).
 __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
                                                    uint32_t mask, int rotate, int adaptive, MatScalars* sc,
-                                                   int slot_n, int slot_m, QOut qx, QOut qxt) {
+                                                   int slot_n, int slot_m, QOut qx, QOut qxt, uint32_t reset_mask) {
   // rows padded to 68 floats: 16-byte row slices for the row blocks, and the
   // 16 lanes of one 128-bit access (4 rows x 4 slices) or 64 consecutive
   // columns of one row fall in distinct banks
@@ -609,9 +630,16 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
   const float* X = x + b * x_bstride;
   const float sgn = tensor_scale_from_amax(amax_read(sc[b], slot_n));
   const float sgm = tensor_scale_from_amax(amax_read(sc[b], slot_m));
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    sc[b].sg[slot_n] = sgn;
-    sc[b].sg[slot_m] = sgm;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x == 0) {
+      sc[b].sg[slot_n] = sgn;
+      sc[b].sg[slot_m] = sgm;
+    }
+    // amax slots the next kernels record into (this kernel reads only slot_n, slot_m)
+    if (threadIdx.x < kAmaxSpread * kNumSlots) {
+      const int line = (int)threadIdx.x / kNumSlots, slot = (int)threadIdx.x % kNumSlots;
+      if ((reset_mask >> slot) & 1u) sc[b].amax[line].v[slot] = 0u;
+    }
   }
   {
     const int i = threadIdx.x >> 2, q = threadIdx.x & 3;   // row i, 16 columns at 16 q
@@ -728,10 +756,12 @@ hipError_t launch_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_
 
 hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
                             uint32_t sign_mask, bool rotate, bool adaptive46, MatScalars* sc,
-                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st) {
+                            int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st,
+                            uint32_t reset_mask) {
+  if (reset_mask & ((1u << slot_n) | (1u << slot_m))) return hipErrorInvalidValue;
   const dim3 grid((uint32_t)(cdiv(m, kT) * cdiv(n, kT)), (uint32_t)batch);
   hipLaunchKernelGGL(k_encode_x2, grid, dim3(256), 0, st, x, m, n, x_bstride, sign_mask, (int)rotate,
-                     (int)adaptive46, sc, slot_n, slot_m, qx, qxt);
+                     (int)adaptive46, sc, slot_n, slot_m, qx, qxt, reset_mask);
   return hipGetLastError();
 }
 
@@ -751,6 +781,8 @@ hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotat
 hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st) {
+  // two-stage records need row-direction chain records over whole stage pairs
+  if (out.rho8 && (axis != 1 || !out.rhog || in.cols % 128 != 0)) return hipErrorInvalidValue;
   const int64_t nblk = in.rows * in.cols / 16;
   const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
   if (axis == 1)
