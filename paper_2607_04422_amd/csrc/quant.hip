@@ -339,28 +339,50 @@ __global__ __launch_bounds__(256) void k_prep_copy(MatChunk ch, MatScalars* sc, 
   const MatDesc& d = ch.m[mi];
   const bool tall = d.rows > d.cols;
   const int64_t xm = tall ? d.cols : d.rows, xn = tall ? d.rows : d.cols;   // canonical m x n
-  const int64_t tcols = cdiv(xn, kT);
-  const int64_t tt = t - d.tile_begin;
-  const int64_t xr0 = (tt / tcols) * kT, xc0 = (tt % tcols) * kT;   // canonical tile origin
+  const uint32_t tcols = (uint32_t)cdiv(xn, kT), tt = (uint32_t)(t - d.tile_begin);
+  const int64_t xr0 = (int64_t)(tt / tcols) * kT, xc0 = (int64_t)(tt % tcols) * kT;   // canonical tile origin
   float* X = xbase + (int64_t)mi * x_bstride;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;   // 64 x 4
   const float tau = sc[mi].tau;
   const float inv = sc[mi].inv_norm;
-  // tile[i][j] = canonical X[xr0 + i][xc0 + j]
-  for (int i = ty; i < kT; i += 4) {
+  // tile[i][j] = canonical X[xr0 + i][xc0 + j]; 16-byte accesses of M and X (rows of
+  // both are 16-byte aligned and m, n are multiples of 16): thread -> four quads
+  // v = threadIdx.x + 256 k, row v / 16 of the tile, columns 4 (v % 16) .. + 3
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int v = (int)threadIdx.x + 256 * k, i = v >> 4, q = v & 15;
     if (!tall) {
-      const int64_t r = xr0 + i, c = xc0 + tx;
-      if (r < xm && c < xn) tile[i][tx] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
+      const int64_t r = xr0 + i, c = xc0 + 4 * q;
+      if (r < xm && c < xn) {
+        float4 a = *reinterpret_cast<const float4*>(d.in + r * d.ld_in + c);
+        a.x = fminf(fmaxf(a.x, -tau), tau) * inv;
+        a.y = fminf(fmaxf(a.y, -tau), tau) * inv;
+        a.z = fminf(fmaxf(a.z, -tau), tau) * inv;
+        a.w = fminf(fmaxf(a.w, -tau), tau) * inv;
+        *reinterpret_cast<float4*>(X + r * xn + c) = a;
+        tile[i][4 * q] = a.x; tile[i][4 * q + 1] = a.y; tile[i][4 * q + 2] = a.z; tile[i][4 * q + 3] = a.w;
+      }
     } else {
-      // M row (xc0 + i), M column (xr0 + tx)  ->  X[xr0 + tx][xc0 + i]
-      const int64_t r = xc0 + i, c = xr0 + tx;
-      if (r < d.rows && c < d.cols) tile[tx][i] = fminf(fmaxf(d.in[r * d.ld_in + c], -tau), tau) * inv;
+      // M row xc0 + i, M columns xr0 + 4q .. + 3  ->  X rows xr0 + 4q .. + 3, column xc0 + i
+      const int64_t r = xc0 + i, c = xr0 + 4 * q;
+      if (r < d.rows && c < d.cols) {
+        const float4 a = *reinterpret_cast<const float4*>(d.in + r * d.ld_in + c);
+        tile[4 * q][i] = fminf(fmaxf(a.x, -tau), tau) * inv;
+        tile[4 * q + 1][i] = fminf(fmaxf(a.y, -tau), tau) * inv;
+        tile[4 * q + 2][i] = fminf(fmaxf(a.z, -tau), tau) * inv;
+        tile[4 * q + 3][i] = fminf(fmaxf(a.w, -tau), tau) * inv;
+      }
     }
   }
   __syncthreads();
-  for (int i = ty; i < kT; i += 4) {
-    const int64_t r = xr0 + i, c = xc0 + tx;
-    if (r < xm && c < xn) X[r * xn + c] = tile[i][tx];
+  if (tall) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int v = (int)threadIdx.x + 256 * k, i = v >> 4, q = v & 15;
+      const int64_t r = xr0 + i, c = xc0 + 4 * q;
+      if (r < xm && c < xn)
+        *reinterpret_cast<float4*>(X + r * xn + c) =
+            make_float4(tile[i][4 * q], tile[i][4 * q + 1], tile[i][4 * q + 2], tile[i][4 * q + 3]);
+    }
   }
   // rotated amaxes: thread -> one 16-column block and one 16-row block of the tile
   float mr = 0.0f, mc = 0.0f;
