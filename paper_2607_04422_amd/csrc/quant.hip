@@ -430,27 +430,40 @@ __global__ __launch_bounds__(256) void k_copy_out(MatChunk ch, const float* xbas
   const int mi = find_matrix(ch, t);
   const MatDesc& d = ch.m[mi];
   const bool tall = d.rows > d.cols;
-  const int64_t tcols = cdiv(d.cols, kT);
-  const int64_t tt = t - d.tile_begin;
-  const int64_t br = (tt / tcols) * kT, bc = (tt % tcols) * kT;   // tile origin in M coordinates
+  const uint32_t tcols = (uint32_t)cdiv(d.cols, kT), tt = (uint32_t)(t - d.tile_begin);
+  const int64_t br = (int64_t)(tt / tcols) * kT, bc = (int64_t)(tt % tcols) * kT;   // tile origin in M coordinates
   const float* X = xbase + (int64_t)mi * x_bstride;
   const int64_t xld = tall ? d.rows : d.cols;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  // 16-byte accesses (see k_prep_copy): thread -> quads v = threadIdx.x + 256 k,
+  // row v / 16 of the tile, columns 4 (v % 16) .. + 3
   if (!tall) {
-    for (int i = ty; i < kT; i += 4) {
-      const int64_t r = br + i, c = bc + tx;
-      if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = X[r * xld + c];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int v = (int)threadIdx.x + 256 * k, i = v >> 4, q = v & 15;
+      const int64_t r = br + i, c = bc + 4 * q;
+      if (r < d.rows && c < d.cols)
+        *reinterpret_cast<float4*>(d.out + r * d.ld_out + c) = *reinterpret_cast<const float4*>(X + r * xld + c);
     }
     return;
   }
-  for (int i = ty; i < kT; i += 4) {
-    const int64_t c = bc + i, r = br + tx;
-    if (r < d.rows && c < d.cols) tile[tx][i] = X[c * xld + r];
+  // X row bc + i, X columns br + 4q .. + 3  ->  M rows br + 4q .. + 3, column bc + i
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int v = (int)threadIdx.x + 256 * k, i = v >> 4, q = v & 15;
+    const int64_t c = bc + i, r = br + 4 * q;
+    if (r < d.rows && c < d.cols) {
+      const float4 a = *reinterpret_cast<const float4*>(X + c * xld + r);
+      tile[4 * q][i] = a.x; tile[4 * q + 1][i] = a.y; tile[4 * q + 2][i] = a.z; tile[4 * q + 3][i] = a.w;
+    }
   }
   __syncthreads();
-  for (int i = ty; i < kT; i += 4) {
-    const int64_t r = br + i, c = bc + tx;
-    if (r < d.rows && c < d.cols) d.out[r * d.ld_out + c] = tile[i][tx];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int v = (int)threadIdx.x + 256 * k, i = v >> 4, q = v & 15;
+    const int64_t r = br + i, c = bc + 4 * q;
+    if (r < d.rows && c < d.cols)
+      *reinterpret_cast<float4*>(d.out + r * d.ld_out + c) =
+          make_float4(tile[i][4 * q], tile[i][4 * q + 1], tile[i][4 * q + 2], tile[i][4 * q + 3]);
   }
 }
 

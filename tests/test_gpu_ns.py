@@ -135,6 +135,21 @@ def test_orthogonalize_default_coeffs_and_zero_steps():
     assert rel_fro(np_(out), ref) <= TOL
 
 
+def test_orthogonalize_large_group_copy_out():
+    """More than 32 matrices of one shape are written back by the copy-out kernel
+    (tall ones transposed back): exact at zero steps, the oracle's NS after five."""
+    mats = [workloads.matrix(96, 32, seed=50 + i) for i in range(40)]
+    mats += [workloads.matrix(32, 64, seed=90 + i) for i in range(36)]
+    ins = [torch.from_numpy(m).cuda() for m in mats]
+    out0 = F.fp4root_orthogonalize(ins, steps=0)
+    for i in (0, 17, 39, 40, 75):
+        x_ref, tall, _ = ns.prepare(mats[i])
+        assert np.array_equal(np_(out0[i]), x_ref.T if tall else x_ref), i
+    outs = F.fp4root_orthogonalize(ins, steps=5, coeffs=MIXED)
+    for i in (0, 39, 40, 75):
+        assert rel_fro(np_(outs[i]), ns.orthogonalize(mats[i], MIXED, seed=0)) <= TOL, i
+
+
 def test_in_place_and_determinism():
     m = workloads.matrix(256, 512, seed=31)
     x1 = torch.from_numpy(m).cuda()
