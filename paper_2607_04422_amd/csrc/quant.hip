@@ -816,8 +816,10 @@ hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotat
 hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st) {
-  // two-stage records need row-direction chain records over whole stage pairs
-  if (out.rho8 && (axis != 1 || !out.rhog || in.cols % 128 != 0)) return hipErrorInvalidValue;
+  // chain records: row blocks over whole 64-column stages (two-stage records over
+  // whole stage pairs)
+  if (out.rhog && (axis != 1 || in.cols % 64 != 0 || in.rows % 16 != 0)) return hipErrorInvalidValue;
+  if (out.rho8 && (!out.rhog || in.cols % 128 != 0)) return hipErrorInvalidValue;
   const int64_t nblk = in.rows * in.cols / 16;
   const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
   if (axis == 1)
