@@ -19,6 +19,9 @@ Plain, slow, obviously-correct NumPy code written from the paper:
 * ``ns``       - Frobenius normalisation and the quantised / unquantised
                  Newton-Schulz recurrence (Section 2 "Root optimizer", Section 3.4
                  display equation).
+* ``momentum`` - the first moment kept in NVFP4 with Hadamard mixing, stochastic
+                 rounding and adaptive 4/6 (Section 3.3 storage recipe, Section 2
+                 "AdamW optimizer" update), the input of the NS orthogonalisation.
 
 Floating point: the quantiser is emulated exactly in binary32 (NumPy float32
 arithmetic, which rounds each operation to nearest-even and never fuses), the

@@ -59,3 +59,22 @@ def rotate_blocks_f32(blocks: np.ndarray, signs: np.ndarray) -> np.ndarray:
         u = np.stack([a + b, a - b], axis=-2).reshape(lead + (16,)).astype(np.float32)
         h *= 2
     return (u * np.float32(0.25)).astype(np.float32)
+
+
+def unrotate_blocks_f32(blocks: np.ndarray, signs: np.ndarray) -> np.ndarray:
+    """Apply (H_16^r)^-1 to every 16-vector in the last axis, in binary32.
+
+    (diag(d) H_16 / 4)^-1 = (H_16 / 4) diag(d), because H_16 H_16 = 16 I: the
+    unsigned butterfly (strides 1, 2, 4, 8, each pair rounded to binary32), then
+    * 0.25, then the signs d.
+    """
+    u = np.asarray(blocks, dtype=np.float32)
+    lead = u.shape[:-1]
+    h = 1
+    while h < 16:
+        v = u.reshape(lead + (16 // (2 * h), 2, h))
+        a = v[..., 0, :]
+        b = v[..., 1, :]
+        u = np.stack([a + b, a - b], axis=-2).reshape(lead + (16,)).astype(np.float32)
+        h *= 2
+    return ((u * np.float32(0.25)).astype(np.float32) * signs.astype(np.float32)).astype(np.float32)
