@@ -69,6 +69,7 @@ enum {
   FP4ROOT_F_HADAMARD = 2u,    /* apply the random 16x16 Hadamard rotation (Section 3.4)      */
   FP4ROOT_F_ADAPTIVE46 = 4u,  /* adaptive 4/6 block scaling (Section 3.4)                    */
   FP4ROOT_F_BF16_PATH = 8u,   /* plain BF16 Newton-Schulz instead of NVFP4 (comparison path) */
+  FP4ROOT_F_STOCHASTIC = 16u, /* stochastic rounding of element codes (momentum state only)  */
   FP4ROOT_F_DEFAULT = 7u      /* CLIP | HADAMARD | ADAPTIVE46: the paper's route             */
 };
 
@@ -156,6 +157,49 @@ int fp4root_ns_step(float* x, int64_t batch, int64_t m, int64_t n, int64_t batch
 int fp4root_orthogonalize(const fp4root_matrix* mats, int64_t count,
                           const fp4root_ns_config* cfg, void* ws, size_t ws_bytes,
                           void* stream);
+
+/* ---- NVFP4 first-moment state ------------------------------------------------ */
+
+/* Workspace bytes fp4root_momentum_update needs (at least 256), or 0 for a bad shape. */
+size_t fp4root_momentum_workspace(int64_t batch, int64_t rows, int64_t cols);
+
+/* One optimizer step of the first moment kept in NVFP4 (Section 3.3: the first
+ * moment is stored in NVFP4 after 16-element Hadamard mixing, with stochastic
+ * rounding and adaptive 4/6 scaling; Section 2 "AdamW optimizer" for the update
+ * m_t = b1 m_{t-1} + (1 - b1) g_t; Section 3.4 feeds m_t to the NVFP4 Root
+ * iteration).  For each of `batch` matrices of rows x cols:
+ *   1. step > 0: m_hat = decode of the state S_{step-1}: u = fl32(q s s_g), then
+ *      the inverse rotation (diag(d) H_16 / 4)^-1 = (H_16 / 4) diag(d) in binary32
+ *      (butterfly strides 1, 2, 4, 8, then * 1/4, then the signs) with the signs
+ *      of step - 1; step = 0: m_hat = 0 and the state is not read;
+ *   2. m_t = fl32(b1 m_hat + b2 g) with b1 = beta, b2 = fl32(1 - beta), the
+ *      products exact and their sum rounded once in binary64;
+ *   3. m_t is written to `m` (FP32): the input of fp4root_orthogonalize;
+ *   4. S_step = the NVFP4 record of m_t along rows, exactly as fp4root_quantize
+ *      makes it (axis 1, rotation with the signs of step `step` when
+ *      FP4ROOT_F_HADAMARD, 4/6 choice by the round-to-nearest errors when
+ *      FP4ROOT_F_ADAPTIVE46), except that with FP4ROOT_F_STOCHASTIC each
+ *      magnitude rounds stochastically with the chosen scale r = fl32(s s_g):
+ *      with x = |u| / r exact and lo <= x < hi neighbours on the E2M1 grid, it
+ *      rounds up to hi iff rho 2^-24 < (x - lo) / (hi - lo) (x >= 6 gives 6,
+ *      r = 0 gives 0, the sign bit is kept), rho = SplitMix64 output e + 1 of
+ *      state SplitMix64(seed ^ 0x5352, step + 1), shifted right by 40 bits, for
+ *      the element at flat index e = (b rows + i) cols + j.
+ * Signs d of step t: bit i of SplitMix64 output t + 1 of state `seed` set means
+ * d_i = -1 (the rule of the NS steps).
+ *   g, m:   device, batch x rows x cols FP32, contiguous (row stride cols, matrix
+ *           stride rows*cols), 16-byte aligned; m may equal g;
+ *   codes, scales, tensor_scale: device, the state in the layout of
+ *           fp4root_quantize (batch x rows x cols/2 bytes, batch x rows x cols/16
+ *           bytes, batch floats), read (step > 0) and then overwritten;
+ *   beta:   in [0, 1]; flags: FP4ROOT_F_HADAMARD | FP4ROOT_F_ADAPTIVE46 |
+ *           FP4ROOT_F_STOCHASTIC; step >= 0.
+ * rows and cols must be multiples of 16.  A NaN or Inf in g is recorded in the
+ * workspace status (fp4root_device_status). */
+int fp4root_momentum_update(const float* g, float* m, int64_t batch, int64_t rows, int64_t cols,
+                            uint8_t* codes, uint8_t* scales, float* tensor_scale, float beta,
+                            uint32_t flags, uint64_t seed, int32_t step, void* ws, size_t ws_bytes,
+                            void* stream);
 
 /* ---- helpers --------------------------------------------------------------- */
 

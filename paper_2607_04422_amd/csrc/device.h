@@ -65,6 +65,40 @@ FP4R_DEV void rotate16(float (&u)[16], uint32_t mask) {
   quarter16(u);
 }
 
+// Inverse of rotate16: (diag(d) H / 4)^-1 = (H / 4) diag(d) since H H = 16 I, i.e.
+// the unsigned butterfly (strides 1, 2, 4, 8, binary32), then * 1/4, then the signs.
+FP4R_DEV void unrotate16(float (&u)[16], uint32_t mask) {
+#pragma unroll
+  for (int h = 1; h < 16; h <<= 1) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if ((i & h) == 0) {
+        const float p = u[i], q = u[i + h];
+        u[i] = p + q;
+        u[i + h] = p - q;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) u[i] = (u[i] * 0.25f) * sign_factor(mask, i);
+}
+
+// SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): output `index` (1-based) of the
+// generator started at `state`.
+FP4R_DEV uint64_t splitmix64_at(uint64_t state, uint64_t index) {
+  uint64_t z = state + 0x9E3779B97F4A7C15ull * index;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Binary32 value of an E4M3FN code (bit 7 ignored): (8 + m) 2^(e - 10), or m 2^-9
+// for the subnormal codes.
+FP4R_DEV float e4m3_value(uint32_t code) {
+  const uint32_t e = (code >> 3) & 15u, m = code & 7u;
+  return e ? __uint_as_float(((e + 120u) << 23) | (m << 20)) : (float)m * 0.001953125f;
+}
+
 // The largest magnitude over a block after rotate16, times 4: the same butterfly
 // up to the last stage, whose pair (fl(p + q), fl(p - q)) has the larger magnitude
 // fl(|p| + |q|).  Multiplying the result by 1/4 gives max |rotate16(u)| exactly

@@ -142,6 +142,21 @@ hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rot
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st);
 
+// launch_encode along rows (axis 1, no clipping, no chain records) with the element
+// magnitudes rounded stochastically (fp4root_momentum_update); draws from `sr_key`.
+hipError_t launch_encode_sr(const Batch& in, uint32_t sign_mask, bool rotate, bool adaptive46,
+                            MatScalars* sc, int slot, const QOut& out, float* tensor_scale,
+                            uint64_t sr_key, hipStream_t st);
+
+// First-moment update of a batch of contiguous rows x cols matrices (matrix
+// stride rows*cols): m = fl32(b1 decode(previous state) + b2 g) (previous state
+// read only when has_prev, decoded with prev_mask), amax of m rotated with `mask`
+// into amax slot 0 of sc[b]; non-finite g sets the status word.
+hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t rows, int64_t cols,
+                             const uint8_t* codes, const uint8_t* scales, const float* prev_sg,
+                             bool has_prev, uint32_t prev_mask, uint32_t mask, bool rotate, float b1,
+                             float b2, MatScalars* sc, uint32_t* status, hipStream_t st);
+
 // Both quantisations of X (m x n, row stride n) from one read: qX along n into
 // qx (slot_n), qXt along m into qxt (slot_m, stored transposed).
 // reset_mask: amax slots of every matrix set to zero by the launch (for the

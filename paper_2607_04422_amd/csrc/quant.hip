@@ -564,10 +564,50 @@ __global__ __launch_bounds__(256) void k_amax(Batch in, uint32_t mask, int rotat
   }
 }
 
-template <int AXIS>
+// E2M1 magnitude of index 0..7 (the hardware decode of the code, exact).
+FP4R_DEV double e2m1_grid(uint32_t idx) {
+  return (double)__builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(idx, 1.0f, 0)).x;
+}
+
+// Stochastic rounding of one block's magnitudes (the first-moment state; see
+// fp4root_momentum_update): u holds kf times the rotated block, `scale` is the
+// chosen E4M3 code and `rtn` the round-to-nearest codes with that scale; element
+// i draws SplitMix64 output e0 + i + 1 of `key`.  With x = |u| / r exact
+// (r = fl32(s s_g)), the floor grid point of x is the nearest one or the one
+// below it (the round-to-nearest quotient is within one ulp of x), and
+// rho (hi - lo) r < (|u| - lo r) 2^24 is exact in binary64 (every term has at
+// most 48 significant bits; |u| - lo r is a difference of numbers within a factor 2).
+FP4R_DEV uint64_t sr_block_codes(const float (&u)[16], float kf, uint32_t scale, float sg, uint64_t rtn,
+                                 uint64_t key, uint64_t e0) {
+  const float r = e4m3_value(scale) * sg;
+  if (!(r > 0.0f)) return rtn & 0x8888888888888888ull;   // magnitudes 0, signs kept
+  const double rd = (double)r;
+  uint64_t out = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float ui = kf == 1.0f ? u[i] : u[i] * 0.25f;
+    const double a = (double)fabsf(ui);
+    const uint32_t c = (uint32_t)(rtn >> (4 * i)) & 15u;
+    uint32_t idx = c & 7u;
+    double lo = e2m1_grid(idx);
+    if (idx > 0 && lo * rd > a) {
+      --idx;
+      lo = e2m1_grid(idx);
+    }
+    if (idx < 7) {
+      const double hi = e2m1_grid(idx + 1);
+      const uint32_t rho = (uint32_t)(splitmix64_at(key, e0 + (uint64_t)i + 1) >> 40);
+      if ((double)rho * (hi - lo) * rd < (a - lo * rd) * 16777216.0) ++idx;
+    }
+    out |= (uint64_t)((c & 8u) | idx) << (4 * i);
+  }
+  return out;
+}
+
+template <int AXIS, bool SR = false>
 __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rotate, int clip,
                                                 int adaptive, MatScalars* sc, int slot, QOut out,
-                                                float* tensor_scale) {
+                                                float* tensor_scale, uint64_t sr_key = 0) {
   const int64_t b = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t nblk = in.rows * in.cols / 16;
@@ -615,6 +655,8 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
     uint64_t codes;
     uint32_t n2;
     quant_block(u, sg, adaptive != 0, scale, codes, n2, want_rho, kf);
+    if constexpr (SR)
+      codes = sr_block_codes(u, kf, scale, sg, codes, sr_key, (uint64_t)((b * in.rows + r) * in.cols + c));
     if (want_rho) {
       rrow = quad_stage_rho(n2, block_exp(scale), &emin);
       if (out.rowst && (threadIdx.x & 3) == 0)
@@ -823,11 +865,107 @@ hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rot
   const int64_t nblk = in.rows * in.cols / 16;
   const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
   if (axis == 1)
-    hipLaunchKernelGGL(k_encode<1>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
-                       (int)adaptive46, sc, slot, out, tensor_scale);
+    hipLaunchKernelGGL((k_encode<1, false>), grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
+                       (int)adaptive46, sc, slot, out, tensor_scale, (uint64_t)0);
   else
-    hipLaunchKernelGGL(k_encode<0>, grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
-                       (int)adaptive46, sc, slot, out, tensor_scale);
+    hipLaunchKernelGGL((k_encode<0, false>), grid, dim3(256), 0, st, in, sign_mask, (int)rotate, (int)clip,
+                       (int)adaptive46, sc, slot, out, tensor_scale, (uint64_t)0);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode_sr(const Batch& in, uint32_t sign_mask, bool rotate, bool adaptive46,
+                            MatScalars* sc, int slot, const QOut& out, float* tensor_scale,
+                            uint64_t sr_key, hipStream_t st) {
+  if (out.rhog) return hipErrorInvalidValue;
+  const int64_t nblk = in.rows * in.cols / 16;
+  const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
+  hipLaunchKernelGGL((k_encode<1, true>), grid, dim3(256), 0, st, in, sign_mask, (int)rotate, 0,
+                     (int)adaptive46, sc, slot, out, tensor_scale, sr_key);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// First-moment update: one thread per 16-element row block of a contiguous
+// matrix.  Decodes the previous NVFP4 state (one rounding of q s s_g, then the
+// inverse rotation), forms m = fl32(b1 m_hat + b2 g) (exact products, one binary64
+// rounding, then binary32), writes m and records the amax of m rotated with
+// `mask` (the tensor scale of the next state) in amax slot 0.
+__global__ __launch_bounds__(256) void k_mom_update(const float* g, float* m, int64_t rows, int64_t cols,
+                                                    const uint8_t* codes, const uint8_t* scales,
+                                                    const float* prev_sg, int has_prev, uint32_t prev_mask,
+                                                    uint32_t mask, int rotate, float b1, float b2,
+                                                    MatScalars* sc, uint32_t* status) {
+  __shared__ float red[4];
+  const int64_t b = blockIdx.y;
+  const int64_t blk = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nblk = rows * cols / 16;
+  float amax = 0.0f;
+  if (blk < nblk) {
+    const int64_t e0 = b * rows * cols + blk * 16;
+    float x[16];
+    const float4* gp = reinterpret_cast<const float4*>(g + e0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = gp[q];
+      x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+    }
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) ok = ok && ((__float_as_uint(x[i]) & 0x7F800000u) != 0x7F800000u);
+    if (!ok) atomicOr(status, kStatusNonFinite);
+    float mh[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mh[i] = 0.0f;
+    if (has_prev) {
+      const uint2 cw = *reinterpret_cast<const uint2*>(codes + e0 / 2);
+      const float s = e4m3_value(scales[e0 / 16]);
+      const float sgp = prev_sg[b];
+      const uint32_t w[2] = {cw.x, cw.y};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        float2 q;
+        switch (k & 3) {
+          case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 0)); break;
+          case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 1)); break;
+          case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 2)); break;
+          default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 3)); break;
+        }
+        mh[2 * k] = (q.x * s) * sgp;       // q s exact, one rounding
+        mh[2 * k + 1] = (q.y * s) * sgp;
+      }
+      if (rotate) unrotate16(mh, prev_mask);
+    }
+    float mv[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mv[i] = (float)__builtin_fma((double)b1, (double)mh[i], (double)b2 * (double)x[i]);
+    float4* mp = reinterpret_cast<float4*>(m + e0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) mp[q] = make_float4(mv[4 * q], mv[4 * q + 1], mv[4 * q + 2], mv[4 * q + 3]);
+    if (rotate) {
+      amax = 0.25f * rot16_absmax4(mv, mask);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(mv[i]));
+    }
+    if (!ok) amax = 0.0f;
+  }
+  amax = warp_max(amax);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float mm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    amax_record(&sc[b], 0, blockIdx.x, mm);
+  }
+}
+
+hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t rows, int64_t cols,
+                             const uint8_t* codes, const uint8_t* scales, const float* prev_sg,
+                             bool has_prev, uint32_t prev_mask, uint32_t mask, bool rotate, float b1,
+                             float b2, MatScalars* sc, uint32_t* status, hipStream_t st) {
+  const int64_t nblk = rows * cols / 16;
+  const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)batch);
+  hipLaunchKernelGGL(k_mom_update, grid, dim3(256), 0, st, g, m, rows, cols, codes, scales, prev_sg,
+                     (int)has_prev, prev_mask, mask, (int)rotate, b1, b2, sc, status);
   return hipGetLastError();
 }
 

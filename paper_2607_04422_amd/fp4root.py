@@ -24,6 +24,7 @@ F_CLIP = 1
 F_HADAMARD = 2
 F_ADAPTIVE46 = 4
 F_BF16_PATH = 8
+F_STOCHASTIC = 16
 F_DEFAULT = 7
 
 
@@ -80,6 +81,10 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.fp4root_ns_step.restype = ctypes.c_int
     lib.fp4root_orthogonalize.argtypes = [ctypes.POINTER(Matrix), i64, ctypes.POINTER(NsConfig), vp, sz, vp]
     lib.fp4root_orthogonalize.restype = ctypes.c_int
+    lib.fp4root_momentum_workspace.argtypes = [i64, i64, i64]
+    lib.fp4root_momentum_workspace.restype = sz
+    lib.fp4root_momentum_update.argtypes = [vp, vp, i64, i64, i64, vp, vp, vp, f32, u32, u64, i32, vp, sz, vp]
+    lib.fp4root_momentum_update.restype = ctypes.c_int
     lib.fp4root_default_coeffs.argtypes = [i64, i64, i32, ctypes.POINTER(ctypes.c_float)]
     lib.fp4root_default_coeffs.restype = ctypes.c_int
     lib.fp4root_device_status.argtypes = [vp, vp]
@@ -236,6 +241,40 @@ def fp4root_ns_step(x: torch.Tensor, a: float, b: float, c: float,
                                ctypes.byref(tr) if tr is not None else None, _ptr(ws), ws.numel(),
                                _stream(stream)), "fp4root_ns_step")
     return out
+
+
+class MomentumState:
+    """NVFP4 first-moment state of a batch of rows x cols matrices (device tensors):
+    codes (B, rows, cols/2), scales (B, rows, cols/16), tensor_scale (B,)."""
+
+    def __init__(self, batch: int, rows: int, cols: int, device="cuda"):
+        self.codes = torch.zeros((batch, rows, cols // 2), dtype=torch.uint8, device=device)
+        self.scales = torch.zeros((batch, rows, cols // 16), dtype=torch.uint8, device=device)
+        self.tensor_scale = torch.zeros(batch, dtype=torch.float32, device=device)
+        self.ws = workspace(load().fp4root_momentum_workspace(batch, rows, cols), device)
+
+
+def fp4root_momentum_update(g: torch.Tensor, state: MomentumState, beta: float, step: int,
+                            flags: int = F_HADAMARD | F_ADAPTIVE46 | F_STOCHASTIC, seed: int = 0,
+                            m: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """One first-moment step: returns m_t (FP32, shape of g) and re-encodes `state`.
+    g: (rows, cols) or (B, rows, cols) contiguous float32.  See include/fp4root.h."""
+    _need_gpu_f32(g, "g")
+    if not g.is_contiguous():
+        raise ValueError("g must be contiguous")
+    gb = g if g.dim() == 3 else g.unsqueeze(0)
+    B, R, C = gb.shape
+    if tuple(state.codes.shape) != (B, R, C // 2):
+        raise ValueError("state shape does not match g")
+    if m is None:
+        m = torch.empty_like(g)
+    _need_gpu_f32(m, "m")
+    if m.shape != g.shape or not m.is_contiguous():
+        raise ValueError("m must be a contiguous tensor of g's shape")
+    _check(load().fp4root_momentum_update(_ptr(gb), _ptr(m), B, R, C, _ptr(state.codes), _ptr(state.scales),
+                                          _ptr(state.tensor_scale), beta, flags, seed, step, _ptr(state.ws),
+                                          state.ws.numel(), _stream(stream)), "fp4root_momentum_update")
+    return m
 
 
 class Orthogonalizer:
