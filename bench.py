@@ -13,8 +13,10 @@ synthetic momentum (Student-t(4) entries, lognormal(0,1) row scales).
 
 Prints ONE JSON line.  Also reports, on the same line: the in-library BF16 NS
 path on the same inputs, a roofline figure for the dominant kernel measured
-with HIP events on its launch stream, and the CPU oracle timed on a bounded
-sample of the same workload.
+with HIP events on its launch stream, the CPU oracle timed on a bounded
+sample of the same workload, and one step of the NVFP4 first-moment state
+(fp4root_momentum_update, Section 3.3 storage recipe) over the same set,
+against the HBM bandwidth (it moves 13.125 algorithmic bytes per element).
 """
 from __future__ import annotations
 
@@ -35,6 +37,7 @@ BF16_MFMA_PEAK_TFLOPS = 2516.6
 # binary32 accumulator, the binary64 folds (2 VALU ops per output per 64-element stage)
 # match that rate too: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz / 2 x 128 FLOP = 2516 TFLOP/s.
 F16_MFMA_PEAK_TFLOPS = BF16_MFMA_PEAK_TFLOPS
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_gemm_fp4_update_block3b_x4_traffic.md")
 
 
@@ -141,6 +144,43 @@ def cpu_baseline(case, coeffs_for, steps, sample_matrices=3):
     }
 
 
+MOM_BYTES_PER_ELEMENT = 4 + 0.5 + 1 / 16 + 4 + 4 + 0.5 + 1 / 16   # update pass + encode pass
+
+
+def momentum_bench(inputs, warmup, iters, torch, F):
+    """One first-moment step (fp4root_momentum_update, stochastic rounding, rotation,
+    4/6) over the whole set, one call per shape batch; inputs act as gradients."""
+    groups = {}
+    for t in inputs:
+        groups.setdefault(tuple(t.shape), []).append(t)
+    batches = []
+    for (r, c), ts in groups.items():
+        g = torch.stack(ts)
+        batches.append((g, F.MomentumState(len(ts), r, c), torch.empty_like(g)))
+    n = sum(g.numel() for g, _, _ in batches)
+    step = [0]
+
+    def run():
+        for g, st, m in batches:
+            F.fp4root_momentum_update(g, st, 0.9, step[0], seed=1, m=m)
+        step[0] += 1
+
+    run()
+    torch.cuda.synchronize()
+    if any(F.fp4root_device_status(st.ws) != 0 for _, st, _ in batches):
+        return {"error": "device status"}
+    calls = []
+    t = time_calls(run, warmup, iters, torch, calls)
+    gbs = n * MOM_BYTES_PER_ELEMENT / t / 1e9
+    out = {"ms_per_step": round(t * 1e3, 4), "per_call_ms": spread(calls), "elements": n,
+           "launches_per_step": 2 * len(batches), "bytes_per_element": MOM_BYTES_PER_ELEMENT,
+           "achieved_GB_per_s": round(gbs, 1), "peak_GB_per_s": HBM_PEAK_GBS,
+           "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+           "flags": "hadamard+adaptive46+stochastic", "beta": 0.9}
+    del batches
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +191,7 @@ def main():
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--no-momentum", action="store_true", help="skip the first-moment state update")
     ap.add_argument("--probe", action="store_true",
                     help="for hardware-counter runs: one warm and one profiled orthogonalize call, "
                          "then a plain 256 MiB device copy as the byte-count reference; no timing")
@@ -251,6 +292,10 @@ def main():
         except Exception as exc:   # context only; never fails the bench line
             bf16["torch_bmm_reference"] = {"error": str(exc)[:200]}
 
+    momentum = None
+    if not args.no_momentum and not args.probe:
+        momentum = momentum_bench(inputs, args.warmup, args.steps, torch, F)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.case, lambda r, c: F.fp4root_default_coeffs(r, c, S), S)
@@ -269,6 +314,7 @@ def main():
         "pct_bf16_mfma_peak": round(100 * tflops / BF16_MFMA_PEAK_TFLOPS, 2),
         "roofline": roofline,
         "bf16_path": bf16,
+        "momentum_state_update": momentum,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -84,12 +84,15 @@ FP4R_DEV void unrotate16(float (&u)[16], uint32_t mask) {
 }
 
 // SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): output `index` (1-based) of the
-// generator started at `state`.
-FP4R_DEV uint64_t splitmix64_at(uint64_t state, uint64_t index) {
-  uint64_t z = state + 0x9E3779B97F4A7C15ull * index;
+// generator started at `state`; splitmix64_mix is its output function applied to
+// the advanced state state + gamma * index.
+FP4R_DEV uint64_t splitmix64_mix(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
   z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
   return z ^ (z >> 31);
+}
+FP4R_DEV uint64_t splitmix64_at(uint64_t state, uint64_t index) {
+  return splitmix64_mix(state + 0x9E3779B97F4A7C15ull * index);
 }
 
 // Binary32 value of an E4M3FN code (bit 7 ignored): (8 + m) 2^(e - 10), or m 2^-9

@@ -582,6 +582,8 @@ FP4R_DEV uint64_t sr_block_codes(const float (&u)[16], float kf, uint32_t scale,
   const float r = e4m3_value(scale) * sg;
   if (!(r > 0.0f)) return rtn & 0x8888888888888888ull;   // magnitudes 0, signs kept
   const double rd = (double)r;
+  // SplitMix64 output e0 + i + 1 starts from key + gamma (e0 + 1) + gamma i
+  const uint64_t z0 = key + 0x9E3779B97F4A7C15ull * (e0 + 1);
   uint64_t out = 0;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -596,7 +598,7 @@ FP4R_DEV uint64_t sr_block_codes(const float (&u)[16], float kf, uint32_t scale,
     }
     if (idx < 7) {
       const double hi = e2m1_grid(idx + 1);
-      const uint32_t rho = (uint32_t)(splitmix64_at(key, e0 + (uint64_t)i + 1) >> 40);
+      const uint32_t rho = (uint32_t)(splitmix64_mix(z0 + 0x9E3779B97F4A7C15ull * (uint64_t)i) >> 40);
       if ((double)rho * (hi - lo) * rd < (a - lo * rd) * 16777216.0) ++idx;
     }
     out |= (uint64_t)((c & 8u) | idx) << (4 * i);
