@@ -67,7 +67,13 @@ CASES = {
     "block3b_x4": "four 3B-shaped decoder blocks (q,k,v,o,gate,up,down), Student-t(4) x per-row "
                   "lognormal(0,1), seed 3, 28 matrices",
     "stress_8192x28672_plus_256x512sq": "one 8192x28672 plus 256 of 512x512, N(0,1), 0.1% x50, seed 4",
+    # the shapes of the paper's isolated Root measurement (Section 4, native-hardware
+    # efficiency: four decoder blocks, d = 4096, d_ff = 11008, 8 KV heads of 128)
+    "paper_d4096_x4": "four d=4096 decoder blocks (q,o 4096x4096; k,v 1024x4096; gate,up 11008x4096; "
+                      "down 4096x11008), Student-t(4) x per-row lognormal(0,1), seed 5, 28 matrices",
 }
+_BLOCK_D4096 = [("q", 4096, 4096), ("k", 1024, 4096), ("v", 1024, 4096), ("o", 4096, 4096),
+                ("gate", 11008, 4096), ("up", 11008, 4096), ("down", 4096, 11008)]
 
 
 def case_shapes(name: str):
@@ -82,6 +88,8 @@ def case_shapes(name: str):
         return [(f"b{b}.{lab}", r, c) for b in range(4) for (lab, r, c) in _BLOCK]
     if name == "stress_8192x28672_plus_256x512sq":
         return [("big", 8192, 28672)] + [(f"s{i}", 512, 512) for i in range(256)]
+    if name == "paper_d4096_x4":
+        return [(f"b{b}.{lab}", r, c) for b in range(4) for (lab, r, c) in _BLOCK_D4096]
     raise KeyError(name)
 
 
@@ -110,6 +118,9 @@ def case_matrices(name: str, limit: int | None = None):
     elif name == "stress_8192x28672_plus_256x512sq":
         rng = _rng(4)
         out = [_normal_outliers(rng, r, c, 50.0) for (_, r, c) in shapes]
+    elif name == "paper_d4096_x4":
+        rng = _rng(5)
+        out = [_t_rows(rng, r, c) for (_, r, c) in shapes]
     return [np.ascontiguousarray(m) for m in out]
 
 
