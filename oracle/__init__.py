@@ -22,6 +22,8 @@ Plain, slow, obviously-correct NumPy code written from the paper:
 * ``momentum`` - the first moment kept in NVFP4 with Hadamard mixing, stochastic
                  rounding and adaptive 4/6 (Section 3.3 storage recipe, Section 2
                  "AdamW optimizer" update), the input of the NS orthogonalisation.
+* ``root_step`` - the parameter update around the orthogonalised momentum
+                 (decoupled weight decay, update scale, BF16 master weights).
 
 Floating point: the quantiser is emulated exactly in binary32 (NumPy float32
 arithmetic, which rounds each operation to nearest-even and never fuses), the
