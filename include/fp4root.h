@@ -201,6 +201,51 @@ int fp4root_momentum_update(const float* g, float* m, int64_t batch, int64_t row
                             uint32_t flags, uint64_t seed, int32_t step, void* ws, size_t ws_bytes,
                             void* stream);
 
+/* ---- the Root step around the orthogonalisation ------------------------------ */
+
+/* Parameter update with the orthogonalised momentum O as the direction (Section 2
+ * "Root optimizer"), decoupled weight decay (training setup: weight decay 0.1) and
+ * BF16 master weights (Section 3.3: no FP32 master copy):
+ *   W <- bf16(fl32(fl32(W c1) - fl32(c2 O))),  c1 = fl32(1 - fl32(lr wd)),  c2 = fl32(lr scale),
+ * bf16() the round-to-nearest-even BF16 of a binary32 value.
+ *   w: device BF16 bit patterns, updated in place; o: device FP32; both `count`
+ *      contiguous elements, 16-byte aligned; count >= 0 a multiple of 8;
+ *   lr, wd, scale: finite. */
+int fp4root_apply_update(uint16_t* w, const float* o, int64_t count, float lr, float wd, float scale,
+                         void* stream);
+
+/* One parameter of a Root step: device pointers to contiguous row-major rows x cols
+ * matrices (16-byte aligned), rows and cols multiples of 16. */
+typedef struct {
+  uint16_t* w;            /* BF16 weights, updated in place                               */
+  const float* g;         /* FP32 gradient                                                */
+  float* m;               /* FP32 scratch: receives m_t, then the orthogonalised O        */
+  uint8_t* m_codes;       /* first-moment state, layout of fp4root_momentum_update (batch 1) */
+  uint8_t* m_scales;
+  float* m_tensor_scale;
+  int64_t rows, cols;
+  float scale;            /* update scale s of this parameter                              */
+} fp4root_param;
+
+typedef struct {
+  float lr, wd, beta;       /* learning rate, decoupled weight decay, first-moment beta1   */
+  uint32_t momentum_flags;  /* FP4ROOT_F_HADAMARD | FP4ROOT_F_ADAPTIVE46 | FP4ROOT_F_STOCHASTIC */
+  uint64_t momentum_seed;   /* parameter p uses seed momentum_seed + p                      */
+  int32_t step;             /* optimizer step t >= 0                                        */
+} fp4root_root_config;
+
+/* Workspace bytes fp4root_root_step needs, or 0 for invalid parameters. */
+size_t fp4root_root_step_workspace(const fp4root_param* params, int64_t count, const fp4root_ns_config* ns);
+
+/* One Root optimizer step over `count` parameters (host arrays; device buffers):
+ * for each parameter p, fp4root_momentum_update of g into m and its state (batch 1,
+ * seed momentum_seed + p); then one fp4root_orthogonalize of every m in place with
+ * `ns` (the p99 clipping, normalisation and NVFP4 NS steps); then
+ * fp4root_apply_update of w with m and the parameter's scale.  A NaN or Inf in a
+ * gradient reaches m and is reported by fp4root_device_status(ws). */
+int fp4root_root_step(const fp4root_param* params, int64_t count, const fp4root_root_config* rc,
+                      const fp4root_ns_config* ns, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- helpers --------------------------------------------------------------- */
 
 /* The library's default per-step coefficients for a rows x cols matrix:

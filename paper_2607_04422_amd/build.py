@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfp4root.so")
-SOURCES = ["quant.hip", "gemm_fp4.hip", "gemm_bf16.hip", "api.cpp"]
+SOURCES = ["quant.hip", "gemm_fp4.hip", "gemm_bf16.hip", "optim.hip", "api.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -95,6 +95,12 @@ FP4R_DEV uint64_t splitmix64_at(uint64_t state, uint64_t index) {
   return splitmix64_mix(state + 0x9E3779B97F4A7C15ull * index);
 }
 
+// Binary32 -> BF16 bit pattern, round to nearest, ties to even (finite inputs).
+FP4R_DEV uint16_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
 // Binary32 value of an E4M3FN code (bit 7 ignored): (8 + m) 2^(e - 10), or m 2^-9
 // for the subnormal codes.
 FP4R_DEV float e4m3_value(uint32_t code) {

@@ -157,6 +157,10 @@ hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t ro
                              bool has_prev, uint32_t prev_mask, uint32_t mask, bool rotate, float b1,
                              float b2, MatScalars* sc, uint32_t* status, hipStream_t st);
 
+// Parameter update W <- bf16(fl32(fl32(W c1) - fl32(c2 O))) over `count` contiguous
+// elements (a multiple of 8; W and O 16-byte aligned).
+hipError_t launch_apply_update(uint16_t* w, const float* o, int64_t count, float c1, float c2, hipStream_t st);
+
 // Both quantisations of X (m x n, row stride n) from one read: qX along n into
 // qx (slot_n), qXt along m into qxt (slot_m, stored transposed).
 // reset_mask: amax slots of every matrix set to zero by the launch (for the

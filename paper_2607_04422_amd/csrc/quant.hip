@@ -974,10 +974,6 @@ hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t ro
 // ---------------------------------------------------------------------------
 // BF16 comparison path: Xb = bf16(X) and Xbt = bf16(X)^T (round to nearest even).
 
-FP4R_DEV uint16_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
 
 __global__ __launch_bounds__(256) void k_cast_bf16(const float* x, int64_t m, int64_t n,
                                                    int64_t x_bstride, uint16_t* xb, uint16_t* xbt,

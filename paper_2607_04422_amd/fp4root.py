@@ -45,6 +45,17 @@ class NsConfig(ctypes.Structure):
                 ("eps", ctypes.c_float), ("seed", ctypes.c_uint64)]
 
 
+class Param(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("g", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("m_codes", ctypes.c_void_p), ("m_scales", ctypes.c_void_p), ("m_tensor_scale", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("scale", ctypes.c_float)]
+
+
+class RootConfig(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("wd", ctypes.c_float), ("beta", ctypes.c_float),
+                ("momentum_flags", ctypes.c_uint32), ("momentum_seed", ctypes.c_uint64), ("step", ctypes.c_int32)]
+
+
 class NsTrace(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "qx_codes", "qx_scales", "qx_sg", "qxt_codes", "qxt_scales", "qxt_sg", "A",
@@ -85,6 +96,13 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.fp4root_momentum_workspace.restype = sz
     lib.fp4root_momentum_update.argtypes = [vp, vp, i64, i64, i64, vp, vp, vp, f32, u32, u64, i32, vp, sz, vp]
     lib.fp4root_momentum_update.restype = ctypes.c_int
+    lib.fp4root_apply_update.argtypes = [vp, vp, i64, f32, f32, f32, vp]
+    lib.fp4root_apply_update.restype = ctypes.c_int
+    lib.fp4root_root_step_workspace.argtypes = [ctypes.POINTER(Param), i64, ctypes.POINTER(NsConfig)]
+    lib.fp4root_root_step_workspace.restype = sz
+    lib.fp4root_root_step.argtypes = [ctypes.POINTER(Param), i64, ctypes.POINTER(RootConfig),
+                                      ctypes.POINTER(NsConfig), vp, sz, vp]
+    lib.fp4root_root_step.restype = ctypes.c_int
     lib.fp4root_default_coeffs.argtypes = [i64, i64, i32, ctypes.POINTER(ctypes.c_float)]
     lib.fp4root_default_coeffs.restype = ctypes.c_int
     lib.fp4root_device_status.argtypes = [vp, vp]
@@ -275,6 +293,75 @@ def fp4root_momentum_update(g: torch.Tensor, state: MomentumState, beta: float, 
                                           _ptr(state.tensor_scale), beta, flags, seed, step, _ptr(state.ws),
                                           state.ws.numel(), _stream(stream)), "fp4root_momentum_update")
     return m
+
+
+def fp4root_apply_update(w: torch.Tensor, o: torch.Tensor, lr: float, wd: float, scale: float, stream=None):
+    """W <- bf16(fl32(fl32(W c1) - fl32(c2 O))) in place on a contiguous bfloat16 tensor w."""
+    if w.dtype != torch.bfloat16 or not w.is_cuda or not w.is_contiguous():
+        raise TypeError("w must be a contiguous bfloat16 GPU tensor")
+    _need_gpu_f32(o, "o")
+    if o.shape != w.shape or not o.is_contiguous():
+        raise ValueError("o must be a contiguous float32 tensor of w's shape")
+    _check(load().fp4root_apply_update(_ptr(w), _ptr(o), w.numel(), lr, wd, scale, _stream(stream)),
+           "fp4root_apply_update")
+
+
+def muon_scale(rows: int, cols: int) -> float:
+    """The update scale sqrt(max(1, rows / cols)) (Muon's shape factor)."""
+    return max(1.0, rows / cols) ** 0.5
+
+
+class RootStep:
+    """Reusable fp4root_root_step over a fixed list of (BF16 weight, FP32 gradient) pairs.
+
+    Holds the descriptors, each parameter's first-moment state and FP32 scratch,
+    the configurations and the workspace; each call is one C call.
+    """
+
+    def __init__(self, weights, grads, lr: float, wd: float = 0.1, beta: float = 0.9, steps: int = 5,
+                 coeffs=None, ns_flags: int = F_DEFAULT, momentum_flags: int = F_HADAMARD | F_ADAPTIVE46 | F_STOCHASTIC,
+                 clip_quantile: float = 0.99, eps: float = 1e-7, seed: int = 0, momentum_seed: int = 0,
+                 scales=None):
+        lib = load()
+        self.weights, self.grads = list(weights), list(grads)
+        n = len(self.weights)
+        self.scratch, self.states = [], []
+        self.params = (Param * max(n, 1))()
+        for i, (w, g) in enumerate(zip(self.weights, self.grads)):
+            if w.dtype != torch.bfloat16 or not w.is_cuda or not w.is_contiguous() or w.dim() != 2:
+                raise TypeError(f"weights[{i}] must be a contiguous 2-D bfloat16 GPU tensor")
+            _need_gpu_f32(g, f"grads[{i}]")
+            if g.shape != w.shape or not g.is_contiguous():
+                raise ValueError(f"grads[{i}] must be contiguous with the weight's shape")
+            r, c = w.shape
+            m = torch.empty_like(g)
+            st = MomentumState(1, r, c, device=w.device)
+            self.scratch.append(m)
+            self.states.append(st)
+            sc = scales[i] if scales is not None else muon_scale(r, c)
+            self.params[i] = Param(w.data_ptr(), g.data_ptr(), m.data_ptr(), st.codes.data_ptr(),
+                                   st.scales.data_ptr(), st.tensor_scale.data_ptr(), r, c, sc)
+        self.count = n
+        if coeffs is not None:
+            flat = [float(v) for row in coeffs for v in row]
+            self._coeffs = (ctypes.c_float * len(flat))(*flat)
+            cptr = ctypes.cast(self._coeffs, ctypes.POINTER(ctypes.c_float))
+        else:
+            self._coeffs, cptr = None, None
+        self.ns = NsConfig(steps, cptr, ns_flags, clip_quantile, eps, seed)
+        self.cfg = RootConfig(lr, wd, beta, momentum_flags, momentum_seed, 0)
+        need = lib.fp4root_root_step_workspace(self.params, n, ctypes.byref(self.ns))
+        if need == 0:
+            raise ValueError("invalid parameters or configuration")
+        self.ws = workspace(need, self.weights[0].device if n else torch.device("cuda"))
+
+    def __call__(self, step: int, stream=None):
+        self.cfg.step = step
+        _check(load().fp4root_root_step(self.params, self.count, ctypes.byref(self.cfg), ctypes.byref(self.ns),
+                                        _ptr(self.ws), self.ws.numel(), _stream(stream)), "fp4root_root_step")
+
+    def status(self, stream=None) -> int:
+        return fp4root_device_status(self.ws, stream)
 
 
 class Orthogonalizer:
