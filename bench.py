@@ -16,7 +16,9 @@ path on the same inputs, a roofline figure for the dominant kernel measured
 with HIP events on its launch stream, the CPU oracle timed on a bounded
 sample of the same workload, and one step of the NVFP4 first-moment state
 (fp4root_momentum_update, Section 3.3 storage recipe) over the same set,
-against the HBM bandwidth (it moves 13.125 algorithmic bytes per element).
+against the HBM bandwidth (it moves 13.125 algorithmic bytes per element), and the
+full Root optimizer step (fp4root_root_step: first moment, NVFP4 Root, BF16
+parameter update) with its update kernel against the HBM bandwidth.
 """
 from __future__ import annotations
 
@@ -181,6 +183,44 @@ def momentum_bench(inputs, warmup, iters, torch, F):
     return out
 
 
+APPLY_BYTES_PER_ELEMENT = 2 + 4 + 2   # BF16 weights in and out, FP32 direction in
+
+
+def root_step_bench(inputs, warmup, iters, torch, F):
+    """The full Root optimizer step (first moment, NVFP4 Root, parameter update) over
+    the set with BF16 weights, and the update kernel alone against HBM bandwidth."""
+    weights = [torch.zeros(t.shape, dtype=torch.bfloat16, device=t.device) for t in inputs]
+    step = F.RootStep(weights, inputs, lr=1.5e-4, wd=0.1, beta=0.9)
+    k = [0]
+
+    def run():
+        step(k[0])
+        k[0] += 1
+
+    run()
+    torch.cuda.synchronize()
+    if step.status() != 0:
+        return {"error": "device status"}
+    calls = []
+    t = time_calls(run, warmup, iters, torch, calls)
+    n = sum(w.numel() for w in weights)
+
+    def apply_all():
+        for w, o in zip(weights, step.scratch):
+            F.fp4root_apply_update(w, o, 1.5e-4, 0.1, 1.0)
+
+    calls_a = []
+    ta = time_calls(apply_all, warmup, iters, torch, calls_a)
+    gbs = n * APPLY_BYTES_PER_ELEMENT / ta / 1e9
+    out = {"ms_per_step": round(t * 1e3, 3), "per_call_ms": spread(calls), "parameters": len(weights),
+           "lr": 1.5e-4, "wd": 0.1, "beta": 0.9, "weights": "bf16",
+           "apply_update": {"ms": round(ta * 1e3, 4), "elements": n, "bytes_per_element": APPLY_BYTES_PER_ELEMENT,
+                            "achieved_GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                            "launches": len(weights)}}
+    del step, weights
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,7 +231,8 @@ def main():
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
-    ap.add_argument("--no-momentum", action="store_true", help="skip the first-moment state update")
+    ap.add_argument("--no-momentum", action="store_true",
+                    help="skip the first-moment state update and the full Root step")
     ap.add_argument("--probe", action="store_true",
                     help="for hardware-counter runs: one warm and one profiled orthogonalize call, "
                          "then a plain 256 MiB device copy as the byte-count reference; no timing")
@@ -293,8 +334,10 @@ def main():
             bf16["torch_bmm_reference"] = {"error": str(exc)[:200]}
 
     momentum = None
+    root = None
     if not args.no_momentum and not args.probe:
         momentum = momentum_bench(inputs, args.warmup, args.steps, torch, F)
+        root = root_step_bench(inputs, args.warmup, args.steps, torch, F)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -315,6 +358,7 @@ def main():
         "roofline": roofline,
         "bf16_path": bf16,
         "momentum_state_update": momentum,
+        "root_optimizer_step": root,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
