@@ -24,6 +24,9 @@ Plain, slow, obviously-correct NumPy code written from the paper:
                  "AdamW optimizer" update), the input of the NS orthogonalisation.
 * ``root_step`` - the parameter update around the orthogonalised momentum
                  (decoupled weight decay, update scale, BF16 master weights).
+* ``qadamw``   - quantized-state AdamW: the first-moment recipe plus the second
+                 moment's square-root / BF16 tile-mean / Hadamard pipeline with
+                 BF16 block scales (Section 3.3), and the AdamW update.
 
 Floating point: the quantiser is emulated exactly in binary32 (NumPy float32
 arithmetic, which rounds each operation to nearest-even and never fuses), the
