@@ -246,6 +246,45 @@ size_t fp4root_root_step_workspace(const fp4root_param* params, int64_t count, c
 int fp4root_root_step(const fp4root_param* params, int64_t count, const fp4root_root_config* rc,
                       const fp4root_ns_config* ns, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- quantized-state AdamW ------------------------------------------------------ */
+
+/* Workspace bytes fp4root_qadamw_update needs for a parameter of n elements, or 0. */
+size_t fp4root_qadamw_workspace(int64_t n);
+
+/* One quantized-state AdamW step of a flat parameter of n elements (Section 3.3:
+ * both moments stored in NVFP4; Section 2 "AdamW optimizer" moments; BF16 master
+ * weights).  n is a positive multiple of 256 (tiles of 256, blocks of 16), at most
+ * 2^25, or a multiple of 4096 up to 2^29.
+ *   1. the first moment exactly as fp4root_momentum_update on a row-major view with
+ *      rows of a multiple of 16 elements (its blocks, draws and codes follow the flat
+ *      index, so the view does not change the state)
+ *      (flags FP4ROOT_F_HADAMARD | FP4ROOT_F_ADAPTIVE46 | FP4ROOT_F_STOCHASTIC, seed,
+ *      step); this step's binary32 m_t is left in m;
+ *   2. the second moment: decode of the previous state (step > 0): u = q s (s the
+ *      BF16 block scale), the inverse rotation with the signs of step - 1, + the BF16
+ *      tile mean, squared (binary32); v_t = fl32(b2 v_hat + fl32(1 - b2) fl32(g g)),
+ *      products exact, one binary64 rounding; the new state: y = sqrt(v_t), BF16 tile
+ *      mean bf16(fl32(S / 256)) of the binary64 tile sum S (each 16-element block
+ *      summed in element order, then the 16 block sums pairwise: a binary tree),
+ *      residual fl32(y - mean), rotation with the signs of step, block scale
+ *      bf16(fl32(bmax / M)) for M = 6 (and 4 with adaptive 4/6, chosen by the
+ *      round-to-nearest binary64 error), E2M1 round-to-nearest codes;
+ *   3. W <- bf16(fl32(fl32(W c1) - fl32(lr upd))), c1 = fl32(1 - fl32(lr wd)),
+ *      upd = fl32(fl32(m_t / bc1) / fl32(fl32(sqrt(fl32(v_t / bc2))) + eps)),
+ *      bc_i = fl32(1 - beta_i^(step+1)) (the power by repeated binary64
+ *      multiplication), IEEE division and square root.
+ *   w: device BF16 bit patterns [n] (in place); g: device FP32 [n]; m: device FP32
+ *   [n] (receives m_t); m_codes [n/2], m_scales [n/16], m_tensor_scale [1]: the
+ *   first-moment state; v_codes [n/2], v_scales [n/16] (BF16), v_means [n/256]
+ *   (BF16): the second-moment state; states are read (step > 0) and overwritten.
+ *   All device buffers 16-byte aligned except the state arrays (8-byte codes).
+ * A NaN or Inf in g is reported through fp4root_device_status(ws). */
+int fp4root_qadamw_update(uint16_t* w, const float* g, float* m, int64_t n, uint8_t* m_codes,
+                          uint8_t* m_scales, float* m_tensor_scale, uint8_t* v_codes, uint16_t* v_scales,
+                          uint16_t* v_means, float lr, float wd, float beta1, float beta2, float eps,
+                          uint32_t flags, uint64_t seed, int32_t step, void* ws, size_t ws_bytes,
+                          void* stream);
+
 /* ---- helpers --------------------------------------------------------------- */
 
 /* The library's default per-step coefficients for a rows x cols matrix:

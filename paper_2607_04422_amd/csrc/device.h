@@ -287,15 +287,13 @@ FP4R_DEV float scale_value(float bmax, float den) {
 // below is kf times its reference value, which is exact (a power-of-two factor on
 // normal numbers), so codes and scale codes are those of the block itself and the
 // error sums are kf^2 times its own.
-FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M, float kf) {
-  BlockCand r;
-  const float s = scale_value(bmax, (M * sg) * kf);
-  const float rs = (s * sg) * kf;
-  r.s = s;
+// Codes and binary32 error sum of a candidate with effective scale rs = s s_g kf
+// (r.s is left to the caller).
+FP4R_DEV void cand_codes(const float (&u)[16], float rs, BlockCand& r) {
   r.s2 = rs * rs;
   r.codes = 0;
   r.err = 0.0f;
-  if (rs > 0.0f && quant_candidate_hw(u, rs, r)) return r;
+  if (rs > 0.0f && quant_candidate_hw(u, rs, r)) return;
   if (rs > 0.0f) {
     // elements next to a grid midpoint: the exact threshold comparisons
     r.codes = 0;
@@ -320,6 +318,13 @@ FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, f
       r.err = fmaf(u[i], u[i], r.err);
     }
   }
+}
+
+FP4R_DEV BlockCand quant_candidate(const float (&u)[16], float bmax, float sg, float M, float kf) {
+  BlockCand r;
+  const float s = scale_value(bmax, (M * sg) * kf);
+  r.s = s;
+  cand_codes(u, (s * sg) * kf, r);
   return r;
 }
 
@@ -399,6 +404,35 @@ FP4R_DEV void quant_block(const float (&u)[16], float sg, bool adaptive, uint32_
   // n2 = 4 k2 M^2 < 2^24: exact in binary32
   const float mant = (float)((scale >> 3) ? 8u + (scale & 7u) : (scale & 7u));
   n2 = (uint32_t)((4.0f * k2) * (mant * mant));
+}
+
+// BF16 value of a bit pattern (exact).
+FP4R_DEV float bf16_value(uint32_t h) { return __uint_as_float((h & 0xFFFFu) << 16); }
+
+// Block quantisation with a BF16 block scale and no tensor scale (the AdamW second
+// moment, Section 3.3): s = bf16(fl32(bmax / M)) for M = 6, and M = 4 with adaptive
+// 4/6; element codes and the 4/6 choice exactly as quant_block (the error bound
+// there holds for any effective scale).  `scale` receives the BF16 bits.
+FP4R_DEV void quant_block_bf16(const float (&u)[16], bool adaptive, uint32_t& scale, uint64_t& codes) {
+  float bmax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, fabsf(u[i]));
+  BlockCand c6;
+  c6.s = bf16_value(bf16_rne(bmax / 6.0f));
+  cand_codes(u, c6.s, c6);
+  if (adaptive) {
+    BlockCand c4;
+    c4.s = bf16_value(bf16_rne(bmax / 4.0f));
+    cand_codes(u, c4.s, c4);
+    const float b = 2.0f * (0x1p-14f * (c4.s2 + c6.s2) + 0x1p-18f * (c4.err + c6.err));
+    bool use4;
+    if (c4.err + b < c6.err) use4 = true;
+    else if (c6.err + b < c4.err) use4 = false;
+    else use4 = cand_err64(u, c4, 1.0f, 1.0f) < cand_err64(u, c6, 1.0f, 1.0f);
+    if (use4) c6 = c4;
+  }
+  scale = bf16_rne(c6.s);
+  codes = c6.codes;
 }
 
 // Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a

@@ -161,6 +161,24 @@ hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t ro
 // elements (a multiple of 8; W and O 16-byte aligned).
 hipError_t launch_apply_update(uint16_t* w, const float* o, int64_t count, float c1, float c2, hipStream_t st);
 
+// Quantized-state AdamW second moment and parameter update over a flat parameter of
+// n elements (a multiple of 256): see k_qadamw.  The first moment m (binary32, this
+// step's) comes from launch_mom_update + the stochastic encoder beforehand.
+struct QAdamWLaunch {
+  uint16_t* w;
+  const float* g;
+  const float* m;
+  uint8_t* vcodes;
+  uint16_t* vscales;
+  uint16_t* vmeans;
+  int64_t n;
+  bool has_prev, rotate, adaptive;
+  uint32_t prev_mask, mask;
+  float b2, c2, bc1, bc2, eps, lr, c1w;
+  uint32_t* status;
+};
+hipError_t launch_qadamw(const QAdamWLaunch& p, hipStream_t st);
+
 // Both quantisations of X (m x n, row stride n) from one read: qX along n into
 // qx (slot_n), qXt along m into qxt (slot_m, stored transposed).
 // reset_mask: amax slots of every matrix set to zero by the launch (for the

@@ -38,4 +38,150 @@ hipError_t launch_apply_update(uint16_t* w, const float* o, int64_t count, float
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Quantized-state AdamW (Section 3.3; Section 2 "AdamW optimizer" moments).  One
+// thread per 16-element block of a flat parameter, so a row of 16 lanes holds one
+// 256-element tile (the parameter length is a multiple of 256 and lanes past the
+// end form whole rows, which compute on a clamped block and store nothing).
+// Per block: decode the previous second-moment state (u = q s, the inverse
+// rotation, + tile mean, squared), v_t = fl32(b2 v_hat + c2 fl32(g g)) (exact
+// products, one binary64 rounding), y = sqrt(v_t); the tile sum of y in binary64
+// (each block in element order, then the 16 block sums pairwise by DPP
+// butterflies: lanes l, l^1, then l^2, then the mirrored half and the mirrored
+// row, each partner sum formed identically in both lanes); the BF16 tile mean,
+// the residual, the rotation and the BF16-scale quantiser; then the AdamW update
+// of the BF16 weights from this step's binary32 m_t and v_t.
+template <int CTRL>
+FP4R_DEV double dpp_d(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = dpp_u<CTRL>((uint32_t)b), hi = dpp_u<CTRL>((uint32_t)(b >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+struct QAdamWArgs {
+  uint16_t* w;
+  const float* g;
+  const float* m;          // this step's binary32 first moment
+  uint8_t* vcodes;         // [N/2]
+  uint16_t* vscales;       // [N/16] BF16
+  uint16_t* vmeans;        // [N/256] BF16
+  int64_t nblk;
+  int has_prev, rotate, adaptive;
+  uint32_t prev_mask, mask;
+  float b2, c2, bc1, bc2, eps, lr, c1w;
+  uint32_t* status;
+};
+
+__global__ __launch_bounds__(256) void k_qadamw(QAdamWArgs a) {
+  const int64_t blk0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool live = blk0 < a.nblk;
+  const int64_t blk = live ? blk0 : a.nblk - 1;
+  const int64_t e0 = blk * 16;
+  float g[16], m[16], vh[16];
+  {
+    const float4* gp = reinterpret_cast<const float4*>(a.g + e0);
+    const float4* mp = reinterpret_cast<const float4*>(a.m + e0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 x = gp[q], y = mp[q];
+      g[4 * q] = x.x; g[4 * q + 1] = x.y; g[4 * q + 2] = x.z; g[4 * q + 3] = x.w;
+      m[4 * q] = y.x; m[4 * q + 1] = y.y; m[4 * q + 2] = y.z; m[4 * q + 3] = y.w;
+    }
+  }
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ok = ok && ((__float_as_uint(g[i]) & 0x7F800000u) != 0x7F800000u);
+  if (live && !ok) atomicOr(a.status, kStatusNonFinite);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) vh[i] = 0.0f;
+  if (a.has_prev) {
+    const uint2 cw = *reinterpret_cast<const uint2*>(a.vcodes + e0 / 2);
+    const float s = bf16_value(a.vscales[blk]);
+    const float mu = bf16_value(a.vmeans[blk >> 4]);
+    const uint32_t wd[2] = {cw.x, cw.y};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      float2 q;
+      switch (k & 3) {
+        case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[k >> 2], 1.0f, 0)); break;
+        case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[k >> 2], 1.0f, 1)); break;
+        case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[k >> 2], 1.0f, 2)); break;
+        default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[k >> 2], 1.0f, 3)); break;
+      }
+      vh[2 * k] = q.x * s;          // exact
+      vh[2 * k + 1] = q.y * s;
+    }
+    if (a.rotate) unrotate16(vh, a.prev_mask);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float y = vh[i] + mu;
+      vh[i] = y * y;
+    }
+  }
+  float v[16], y[16];
+  double bs = 0.0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float gg = g[i] * g[i];
+    v[i] = (float)__builtin_fma((double)a.b2, (double)vh[i], (double)a.c2 * (double)gg);
+    y[i] = __builtin_sqrtf(v[i]);
+    bs += (double)y[i];
+  }
+  bs = bs + dpp_d<0xB1>(bs);    // lanes l, l ^ 1
+  bs = bs + dpp_d<0x4E>(bs);    // l ^ 2
+  bs = bs + dpp_d<0x141>(bs);   // the other quad of the half-row
+  bs = bs + dpp_d<0x140>(bs);   // the other half of the row
+  const uint32_t mu_bits = bf16_rne((float)(bs * (1.0 / 256.0)));
+  const float mu = bf16_value(mu_bits);
+  float u[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) u[i] = y[i] - mu;
+  if (a.rotate) rotate16(u, a.mask);
+  uint32_t sbits;
+  uint64_t codes;
+  quant_block_bf16(u, a.adaptive != 0, sbits, codes);
+  // AdamW on the BF16 weights with this step's moments
+  const uint4* wp = reinterpret_cast<const uint4*>(a.w + e0);
+  const uint4 w0 = wp[0], w1 = wp[1];
+  const uint32_t ww[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+  uint32_t out[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t pair = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = 2 * k + h;
+      const float wv = __uint_as_float(h ? (ww[k] & 0xFFFF0000u) : (ww[k] << 16));
+      const float mh = m[i] / a.bc1;
+      const float den = __builtin_sqrtf(v[i] / a.bc2) + a.eps;
+      const float upd = mh / den;
+      const float t0 = wv * a.c1w, t1 = a.lr * upd;
+      pair |= (uint32_t)bf16_rne(t0 - t1) << (16 * h);
+    }
+    out[k] = pair;
+  }
+  if (live) {
+    uint4* wo = reinterpret_cast<uint4*>(a.w + e0);
+    wo[0] = make_uint4(out[0], out[1], out[2], out[3]);
+    wo[1] = make_uint4(out[4], out[5], out[6], out[7]);
+    *reinterpret_cast<uint2*>(a.vcodes + e0 / 2) = make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+    a.vscales[blk] = (uint16_t)sbits;
+    if ((blk & 15) == 0) a.vmeans[blk >> 4] = (uint16_t)mu_bits;
+  }
+}
+
+hipError_t launch_qadamw(const QAdamWLaunch& p, hipStream_t st) {
+  QAdamWArgs a;
+  a.w = p.w; a.g = p.g; a.m = p.m; a.vcodes = p.vcodes; a.vscales = p.vscales; a.vmeans = p.vmeans;
+  a.nblk = p.n / 16;
+  a.has_prev = p.has_prev; a.rotate = p.rotate; a.adaptive = p.adaptive;
+  a.prev_mask = p.prev_mask; a.mask = p.mask;
+  a.b2 = p.b2; a.c2 = p.c2; a.bc1 = p.bc1; a.bc2 = p.bc2; a.eps = p.eps; a.lr = p.lr; a.c1w = p.c1w;
+  a.status = p.status;
+  if (a.nblk <= 0) return hipSuccess;
+  const dim3 grid((uint32_t)((a.nblk + 255) / 256));
+  hipLaunchKernelGGL(k_qadamw, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 }  // namespace fp4r

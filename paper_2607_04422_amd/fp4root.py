@@ -96,6 +96,11 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.fp4root_momentum_workspace.restype = sz
     lib.fp4root_momentum_update.argtypes = [vp, vp, i64, i64, i64, vp, vp, vp, f32, u32, u64, i32, vp, sz, vp]
     lib.fp4root_momentum_update.restype = ctypes.c_int
+    lib.fp4root_qadamw_workspace.argtypes = [i64]
+    lib.fp4root_qadamw_workspace.restype = sz
+    lib.fp4root_qadamw_update.argtypes = [vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, f32, f32, f32, f32, f32,
+                                          u32, u64, i32, vp, sz, vp]
+    lib.fp4root_qadamw_update.restype = ctypes.c_int
     lib.fp4root_apply_update.argtypes = [vp, vp, i64, f32, f32, f32, vp]
     lib.fp4root_apply_update.restype = ctypes.c_int
     lib.fp4root_root_step_workspace.argtypes = [ctypes.POINTER(Param), i64, ctypes.POINTER(NsConfig)]
@@ -304,6 +309,39 @@ def fp4root_apply_update(w: torch.Tensor, o: torch.Tensor, lr: float, wd: float,
         raise ValueError("o must be a contiguous float32 tensor of w's shape")
     _check(load().fp4root_apply_update(_ptr(w), _ptr(o), w.numel(), lr, wd, scale, _stream(stream)),
            "fp4root_apply_update")
+
+
+class QAdamWState:
+    """Both quantized AdamW moments of a flat parameter of n elements (device tensors)."""
+
+    def __init__(self, n: int, device="cuda"):
+        if n <= 0 or n % 256:
+            raise ValueError("n must be a positive multiple of 256")
+        self.n = n
+        self.m = torch.empty(n, dtype=torch.float32, device=device)
+        self.m_codes = torch.zeros(n // 2, dtype=torch.uint8, device=device)
+        self.m_scales = torch.zeros(n // 16, dtype=torch.uint8, device=device)
+        self.m_tensor_scale = torch.zeros(1, dtype=torch.float32, device=device)
+        self.v_codes = torch.zeros(n // 2, dtype=torch.uint8, device=device)
+        self.v_scales = torch.zeros(n // 16, dtype=torch.int16, device=device)
+        self.v_means = torch.zeros(n // 256, dtype=torch.int16, device=device)
+        self.ws = workspace(load().fp4root_qadamw_workspace(n), device)
+
+
+def fp4root_qadamw_update(w: torch.Tensor, g: torch.Tensor, state: QAdamWState, step: int, lr: float,
+                          wd: float = 0.1, beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-8,
+                          flags: int = F_HADAMARD | F_ADAPTIVE46 | F_STOCHASTIC, seed: int = 0, stream=None):
+    """One quantized-state AdamW step on a flat contiguous bfloat16 parameter w with FP32 gradient g."""
+    if w.dtype != torch.bfloat16 or not w.is_cuda or not w.is_contiguous():
+        raise TypeError("w must be a contiguous bfloat16 GPU tensor")
+    _need_gpu_f32(g, "g")
+    if g.numel() != w.numel() or not g.is_contiguous() or w.numel() != state.n:
+        raise ValueError("g and state must match w")
+    _check(load().fp4root_qadamw_update(
+        _ptr(w), _ptr(g), _ptr(state.m), state.n, _ptr(state.m_codes), _ptr(state.m_scales),
+        _ptr(state.m_tensor_scale), _ptr(state.v_codes), _ptr(state.v_scales), _ptr(state.v_means),
+        lr, wd, beta1, beta2, eps, flags, seed, step, _ptr(state.ws), state.ws.numel(), _stream(stream)),
+        "fp4root_qadamw_update")
 
 
 def muon_scale(rows: int, cols: int) -> float:
