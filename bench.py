@@ -18,7 +18,9 @@ sample of the same workload, and one step of the NVFP4 first-moment state
 (fp4root_momentum_update, Section 3.3 storage recipe) over the same set,
 against the HBM bandwidth (it moves 13.125 algorithmic bytes per element), and the
 full Root optimizer step (fp4root_root_step: first moment, NVFP4 Root, BF16
-parameter update) with its update kernel against the HBM bandwidth.
+parameter update) with its update kernel against the HBM bandwidth, and one
+quantized-state AdamW step (fp4root_qadamw_update) with every matrix as a flat
+parameter, against the HBM bandwidth.
 """
 from __future__ import annotations
 
@@ -221,6 +223,41 @@ def root_step_bench(inputs, warmup, iters, torch, F):
     return out
 
 
+# first-moment pass (update + stochastic encode) + second-moment / weight pass:
+# g 4 + m 4 + w 2 + v state 0.6328 read, v state 0.6328 + w 2 written
+QADAMW_BYTES_PER_ELEMENT = MOM_BYTES_PER_ELEMENT + 4 + 4 + 2 + 2 * (0.5 + 2 / 16 + 2 / 256) + 2
+
+
+def qadamw_bench(inputs, warmup, iters, torch, F):
+    """One quantized-state AdamW step with every matrix of the set as a flat parameter."""
+    params = []
+    for t in inputs:
+        n = t.numel()
+        params.append((torch.zeros(n, dtype=torch.bfloat16, device=t.device), t.reshape(-1), F.QAdamWState(n)))
+    k = [0]
+
+    def run():
+        for w, g, st in params:
+            F.fp4root_qadamw_update(w, g, st, k[0], 1e-4, 0.1, 0.9, 0.95, 1e-8)
+        k[0] += 1
+
+    run()
+    torch.cuda.synchronize()
+    if any(F.fp4root_device_status(st.ws) != 0 for _, _, st in params):
+        return {"error": "device status"}
+    calls = []
+    t = time_calls(run, warmup, iters, torch, calls)
+    n = sum(w.numel() for w, _, _ in params)
+    gbs = n * QADAMW_BYTES_PER_ELEMENT / t / 1e9
+    out = {"ms_per_step": round(t * 1e3, 4), "per_call_ms": spread(calls), "parameters": len(params),
+           "elements": n, "bytes_per_element": round(QADAMW_BYTES_PER_ELEMENT, 4),
+           "achieved_GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+           "state_bits_per_element": {"m": 4.5, "v": 5.0625}, "weights": "bf16",
+           "flags": "hadamard+adaptive46+stochastic (m)"}
+    del params
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,7 +269,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--no-momentum", action="store_true",
-                    help="skip the first-moment state update and the full Root step")
+                    help="skip the first-moment state update, the full Root step and Q-AdamW")
     ap.add_argument("--probe", action="store_true",
                     help="for hardware-counter runs: one warm and one profiled orthogonalize call, "
                          "then a plain 256 MiB device copy as the byte-count reference; no timing")
@@ -335,9 +372,11 @@ def main():
 
     momentum = None
     root = None
+    qadamw = None
     if not args.no_momentum and not args.probe:
         momentum = momentum_bench(inputs, args.warmup, args.steps, torch, F)
         root = root_step_bench(inputs, args.warmup, args.steps, torch, F)
+        qadamw = qadamw_bench(inputs, args.warmup, args.steps, torch, F)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -359,6 +398,7 @@ def main():
         "bf16_path": bf16,
         "momentum_state_update": momentum,
         "root_optimizer_step": root,
+        "qadamw_step": qadamw,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
