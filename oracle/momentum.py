@@ -92,12 +92,16 @@ def decode_state(state: NVFP4, signs: np.ndarray | None) -> np.ndarray:
 
 
 def encode_state(m: np.ndarray, signs: np.ndarray | None, adaptive46: bool,
-                 draws: np.ndarray | None) -> NVFP4:
-    """NVFP4 record of a binary32 momentum; ``draws`` (rows x cols, 24-bit) selects SR."""
+                 draws: np.ndarray | None, rows: np.ndarray | None = None) -> NVFP4:
+    """NVFP4 record of a binary32 momentum; ``draws`` (24-bit, one per element of the
+    encoded rows) selects SR.  ``rows`` (optional) encodes only those rows, with the
+    tensor scale of the whole matrix (as ``quantize``)."""
     m = np.asarray(m, np.float32)
-    rec = quantize(m, axis=1, signs=signs, adaptive46=adaptive46)
+    rec = quantize(m, axis=1, signs=signs, adaptive46=adaptive46, rows=rows)
     if draws is None:
         return rec
+    if rows is not None:
+        m = m[np.asarray(rows, dtype=np.int64)]
     rows, cols = m.shape
     blocks = m.reshape(rows, cols // 16, 16)
     u = rotate_blocks_f32(blocks, signs) if signs is not None else blocks
