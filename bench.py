@@ -223,9 +223,12 @@ def root_step_bench(inputs, warmup, iters, torch, F):
     return out
 
 
-# first-moment pass (update + stochastic encode) + second-moment / weight pass:
-# g 4 + m 4 + w 2 + v state 0.6328 read, v state 0.6328 + w 2 written
-QADAMW_BYTES_PER_ELEMENT = MOM_BYTES_PER_ELEMENT + 4 + 4 + 2 + 2 * (0.5 + 2 / 16 + 2 / 256) + 2
+# pass 1 (first moment read only, second moment, weights): g 4 + m state 0.5625 +
+# v state 0.6328 + w 2 read, v state 0.6328 + w 2 written; pass 2 (first moment
+# re-derived and encoded in place): g 4 + m state 0.5625 read, m state 0.5625 written
+_M_STATE = 0.5 + 1 / 16
+_V_STATE = 0.5 + 2 / 16 + 2 / 256
+QADAMW_BYTES_PER_ELEMENT = (4 + _M_STATE + 2 * _V_STATE + 2 + 2) + (4 + 2 * _M_STATE)
 
 
 def qadamw_bench(inputs, warmup, iters, torch, F):

@@ -257,7 +257,9 @@ size_t fp4root_qadamw_workspace(int64_t n);
  * 2^25, or a multiple of 4096 up to 2^29.
  *   1. the first moment exactly as fp4root_momentum_update on a row-major view with
  *      rows of a multiple of 16 elements (its blocks, draws and codes follow the flat
- *      index, so the view does not change the state)
+ *      index, so the view does not change the state); m_t is written to m when m
+ *      is not NULL (the step itself does not need it: a second pass re-derives m_t
+ *      from g and the previous state to encode the new one)
  *      (flags FP4ROOT_F_HADAMARD | FP4ROOT_F_ADAPTIVE46 | FP4ROOT_F_STOCHASTIC, seed,
  *      step); this step's binary32 m_t is left in m;
  *   2. the second moment: decode of the previous state (step > 0): u = q s (s the
@@ -274,7 +276,7 @@ size_t fp4root_qadamw_workspace(int64_t n);
  *      bc_i = fl32(1 - beta_i^(step+1)) (the power by repeated binary64
  *      multiplication), IEEE division and square root.
  *   w: device BF16 bit patterns [n] (in place); g: device FP32 [n]; m: device FP32
- *   [n] (receives m_t); m_codes [n/2], m_scales [n/16], m_tensor_scale [1]: the
+ *   [n] (receives m_t) or NULL; m_codes [n/2], m_scales [n/16], m_tensor_scale [1]: the
  *   first-moment state; v_codes [n/2], v_scales [n/16] (BF16), v_means [n/256]
  *   (BF16): the second-moment state; states are read (step > 0) and overwritten.
  *   All device buffers 16-byte aligned except the state arrays (8-byte codes).

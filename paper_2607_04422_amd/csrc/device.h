@@ -435,6 +435,38 @@ FP4R_DEV void quant_block_bf16(const float (&u)[16], bool adaptive, uint32_t& sc
   codes = c6.codes;
 }
 
+// The first-moment update of one 16-element block at flat offset e0: decode of the
+// previous state (q s exact, times its tensor scale with one rounding, then the
+// inverse rotation) when has_prev, then m = fl32(b1 m_hat + b2 g) with exact
+// products and one binary64 rounding.
+FP4R_DEV void mom_block(const float (&x)[16], const uint8_t* codes, const uint8_t* scales, int64_t e0,
+                        float sgp, bool has_prev, uint32_t prev_mask, bool rotate, float b1, float b2,
+                        float (&mv)[16]) {
+  float mh[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mh[i] = 0.0f;
+  if (has_prev) {
+    const uint2 cw = *reinterpret_cast<const uint2*>(codes + e0 / 2);
+    const float s = e4m3_value(scales[e0 / 16]);
+    const uint32_t w[2] = {cw.x, cw.y};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      float2 q;
+      switch (k & 3) {
+        case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 0)); break;
+        case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 1)); break;
+        case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 2)); break;
+        default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 3)); break;
+      }
+      mh[2 * k] = (q.x * s) * sgp;       // q s exact, one rounding
+      mh[2 * k + 1] = (q.y * s) * sgp;
+    }
+    if (rotate) unrotate16(mh, prev_mask);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mv[i] = (float)__builtin_fma((double)b1, (double)mh[i], (double)b2 * (double)x[i]);
+}
+
 // Chain bound of one 4-block stage of a row (the NVFP4 products accumulate a
 // stage in binary32 when rho sigma < 2^48, see gemm_fp4.hip):
 //   rho = sum_b n2_b 4^(e_b - e_min),  e = max(exponent field, 1) over blocks with

@@ -64,6 +64,9 @@ __device__ inline uint32_t amax_read(const MatScalars& s, int slot) {
 // update product of step k can record the amaxes of X_{k+1} while step k still
 // reads those of X_k.
 constexpr int kSlotXn = 0, kSlotXm = 1, kSlotA = 4, kSlotB = 5;
+// Quantized-state AdamW: the first moment's new tensor scale lives in slot 0 and the
+// previous one is saved in sg[kSlotPrevState] by the step's first pass.
+constexpr int kSlotPrevState = 1;
 constexpr int kNumSlots = 6;
 
 // Radix select histogram: [2 ranks][2048 bins] per matrix.
@@ -161,13 +164,27 @@ hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t ro
 // elements (a multiple of 8; W and O 16-byte aligned).
 hipError_t launch_apply_update(uint16_t* w, const float* o, int64_t count, float c1, float c2, hipStream_t st);
 
-// Quantized-state AdamW second moment and parameter update over a flat parameter of
-// n elements (a multiple of 256): see k_qadamw.  The first moment m (binary32, this
-// step's) comes from launch_mom_update + the stochastic encoder beforehand.
+// Second pass of a quantized-state AdamW step on a flat parameter of n elements:
+// re-derive m_t from g and the unchanged previous first-moment state and encode it
+// in place (stochastically when sr), tensor scale from amax slot 0 of sc[0].
+hipError_t launch_mom_encode(const float* g, uint8_t* codes, uint8_t* scales, int64_t n, bool has_prev,
+                             uint32_t prev_mask, uint32_t mask, bool rotate, bool adaptive, bool sr, float b1,
+                             float b2, MatScalars* sc, float* tensor_scale, uint64_t sr_key, hipStream_t st);
+
+// First pass of a quantized-state AdamW step over a flat parameter of n elements (a
+// multiple of 256): see k_qadamw.  It forms this step's first moment m_t from the
+// previous first-moment state (read only) and g, records its rotated amax in slot 0
+// of sc[0], saves the previous tensor scale in sc[0].sg[kSlotPrevState], and
+// writes m_t to m_out when that is not null.
 struct QAdamWLaunch {
   uint16_t* w;
   const float* g;
-  const float* m;
+  float* m_out;
+  const uint8_t* mcodes;
+  const uint8_t* mscales;
+  const float* m_prev_sg;
+  float b1, c1m;
+  MatScalars* sc;
   uint8_t* vcodes;
   uint16_t* vscales;
   uint16_t* vmeans;

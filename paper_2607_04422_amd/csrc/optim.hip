@@ -39,11 +39,13 @@ hipError_t launch_apply_update(uint16_t* w, const float* o, int64_t count, float
 }
 
 // ---------------------------------------------------------------------------
-// Quantized-state AdamW (Section 3.3; Section 2 "AdamW optimizer" moments).  One
-// thread per 16-element block of a flat parameter, so a row of 16 lanes holds one
-// 256-element tile (the parameter length is a multiple of 256 and lanes past the
-// end form whole rows, which compute on a clamped block and store nothing).
-// Per block: decode the previous second-moment state (u = q s, the inverse
+// Quantized-state AdamW (Section 3.3; Section 2 "AdamW optimizer" moments), first
+// pass.  One thread per 16-element block of a flat parameter, so a row of 16 lanes
+// holds one 256-element tile (the parameter length is a multiple of 256 and lanes
+// past the end form whole rows, which compute on a clamped block and store nothing).
+// Per block: this step's first moment m_t from the previous first-moment state and
+// g (mom_block; its rotated amax goes to amax slot 0 for the second pass, which
+// re-derives m_t and encodes it); decode the previous second-moment state (u = q s, the inverse
 // rotation, + tile mean, squared), v_t = fl32(b2 v_hat + c2 fl32(g g)) (exact
 // products, one binary64 rounding), y = sqrt(v_t); the tile sum of y in binary64
 // (each block in element order, then the 16 block sums pairwise by DPP
@@ -61,7 +63,12 @@ FP4R_DEV double dpp_d(double v) {
 struct QAdamWArgs {
   uint16_t* w;
   const float* g;
-  const float* m;          // this step's binary32 first moment
+  float* m_out;            // optional: this step's binary32 first moment
+  const uint8_t* mcodes;   // previous first-moment state (read only here)
+  const uint8_t* mscales;
+  const float* m_prev_sg;
+  float b1, c1m;
+  MatScalars* sc;
   uint8_t* vcodes;         // [N/2]
   uint16_t* vscales;       // [N/16] BF16
   uint16_t* vmeans;        // [N/256] BF16
@@ -73,25 +80,51 @@ struct QAdamWArgs {
 };
 
 __global__ __launch_bounds__(256) void k_qadamw(QAdamWArgs a) {
+  __shared__ float red[4];
   const int64_t blk0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const bool live = blk0 < a.nblk;
   const int64_t blk = live ? blk0 : a.nblk - 1;
   const int64_t e0 = blk * 16;
+  const float m_prev_sg = a.has_prev ? a.m_prev_sg[0] : 0.0f;
+  if (blk0 == 0) a.sc->sg[kSlotPrevState] = m_prev_sg;   // for the second pass
   float g[16], m[16], vh[16];
   {
     const float4* gp = reinterpret_cast<const float4*>(a.g + e0);
-    const float4* mp = reinterpret_cast<const float4*>(a.m + e0);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float4 x = gp[q], y = mp[q];
+      const float4 x = gp[q];
       g[4 * q] = x.x; g[4 * q + 1] = x.y; g[4 * q + 2] = x.z; g[4 * q + 3] = x.w;
-      m[4 * q] = y.x; m[4 * q + 1] = y.y; m[4 * q + 2] = y.z; m[4 * q + 3] = y.w;
     }
   }
   bool ok = true;
 #pragma unroll
   for (int i = 0; i < 16; ++i) ok = ok && ((__float_as_uint(g[i]) & 0x7F800000u) != 0x7F800000u);
   if (live && !ok) atomicOr(a.status, kStatusNonFinite);
+  // this step's first moment, and the rotated amax of it for the second pass
+  mom_block(g, a.mcodes, a.mscales, e0, m_prev_sg, a.has_prev != 0, a.prev_mask, a.rotate != 0, a.b1, a.c1m, m);
+  if (live && a.m_out) {
+    float4* mo = reinterpret_cast<float4*>(a.m_out + e0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) mo[q] = make_float4(m[4 * q], m[4 * q + 1], m[4 * q + 2], m[4 * q + 3]);
+  }
+  {
+    float amax = 0.0f;
+    if (a.rotate) {
+      float t[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) t[i] = m[i];
+      amax = 0.25f * rot16_absmax4(t, a.mask);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(m[i]));
+    }
+    if (!live || !ok) amax = 0.0f;
+    amax = warp_max(amax);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0)
+      amax_record(a.sc, 0, blockIdx.x, fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+  }
 #pragma unroll
   for (int i = 0; i < 16; ++i) vh[i] = 0.0f;
   if (a.has_prev) {
@@ -172,7 +205,9 @@ __global__ __launch_bounds__(256) void k_qadamw(QAdamWArgs a) {
 
 hipError_t launch_qadamw(const QAdamWLaunch& p, hipStream_t st) {
   QAdamWArgs a;
-  a.w = p.w; a.g = p.g; a.m = p.m; a.vcodes = p.vcodes; a.vscales = p.vscales; a.vmeans = p.vmeans;
+  a.w = p.w; a.g = p.g; a.m_out = p.m_out; a.mcodes = p.mcodes; a.mscales = p.mscales; a.m_prev_sg = p.m_prev_sg;
+  a.b1 = p.b1; a.c1m = p.c1m; a.sc = p.sc;
+  a.vcodes = p.vcodes; a.vscales = p.vscales; a.vmeans = p.vmeans;
   a.nblk = p.n / 16;
   a.has_prev = p.has_prev; a.rotate = p.rotate; a.adaptive = p.adaptive;
   a.prev_mask = p.prev_mask; a.mask = p.mask;

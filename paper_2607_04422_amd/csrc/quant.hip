@@ -886,6 +886,7 @@ hipError_t launch_encode_sr(const Batch& in, uint32_t sign_mask, bool rotate, bo
   return hipGetLastError();
 }
 
+
 // ---------------------------------------------------------------------------
 // First-moment update: one thread per 16-element row block of a contiguous
 // matrix.  Decodes the previous NVFP4 state (one rounding of q s s_g, then the
@@ -915,31 +916,8 @@ __global__ __launch_bounds__(256) void k_mom_update(const float* g, float* m, in
 #pragma unroll
     for (int i = 0; i < 16; ++i) ok = ok && ((__float_as_uint(x[i]) & 0x7F800000u) != 0x7F800000u);
     if (!ok) atomicOr(status, kStatusNonFinite);
-    float mh[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mh[i] = 0.0f;
-    if (has_prev) {
-      const uint2 cw = *reinterpret_cast<const uint2*>(codes + e0 / 2);
-      const float s = e4m3_value(scales[e0 / 16]);
-      const float sgp = prev_sg[b];
-      const uint32_t w[2] = {cw.x, cw.y};
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        float2 q;
-        switch (k & 3) {
-          case 0: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 0)); break;
-          case 1: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 1)); break;
-          case 2: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 2)); break;
-          default: q = __builtin_bit_cast(float2, __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[k >> 2], 1.0f, 3)); break;
-        }
-        mh[2 * k] = (q.x * s) * sgp;       // q s exact, one rounding
-        mh[2 * k + 1] = (q.y * s) * sgp;
-      }
-      if (rotate) unrotate16(mh, prev_mask);
-    }
     float mv[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mv[i] = (float)__builtin_fma((double)b1, (double)mh[i], (double)b2 * (double)x[i]);
+    mom_block(x, codes, scales, e0, has_prev ? prev_sg[b] : 0.0f, has_prev, prev_mask, rotate, b1, b2, mv);
     float4* mp = reinterpret_cast<float4*>(m + e0);
 #pragma unroll
     for (int q = 0; q < 4; ++q) mp[q] = make_float4(mv[4 * q], mv[4 * q + 1], mv[4 * q + 2], mv[4 * q + 3]);
@@ -958,6 +936,56 @@ __global__ __launch_bounds__(256) void k_mom_update(const float* g, float* m, in
     const float mm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
     amax_record(&sc[b], 0, blockIdx.x, mm);
   }
+}
+
+// Re-encode the first moment of a flat parameter (batch 1, n elements) in place,
+// recomputing m_t = fl32(b1 decode(old state) + b2 g) exactly as mom_block does:
+// the quantized-state AdamW step's second pass (its first pass recorded the rotated
+// amax of m_t in slot 0 and saved the previous tensor scale in sg[kSlotPrevState]).
+// Each thread reads and writes only its own block of the state.
+template <bool SR>
+__global__ __launch_bounds__(256) void k_mom_encode(const float* g, uint8_t* codes, uint8_t* scales,
+                                                    int64_t nblk, int has_prev, uint32_t prev_mask,
+                                                    uint32_t mask, int rotate, int adaptive, float b1, float b2,
+                                                    MatScalars* sc, float* tensor_scale, uint64_t sr_key) {
+  const int64_t blk = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const float sg = tensor_scale_from_amax(amax_read(sc[0], 0));
+  if (blk == 0) {
+    sc[0].sg[0] = sg;
+    tensor_scale[0] = sg;
+  }
+  if (blk >= nblk) return;
+  const int64_t e0 = blk * 16;
+  float x[16];
+  const float4* gp = reinterpret_cast<const float4*>(g + e0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = gp[q];
+    x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+  }
+  float u[16];
+  mom_block(x, codes, scales, e0, sc[0].sg[kSlotPrevState], has_prev != 0, prev_mask, rotate != 0, b1, b2, u);
+  const float kf = rotate_for_quant(u, mask, rotate, sg);
+  uint32_t scale, n2;
+  uint64_t c;
+  quant_block(u, sg, adaptive != 0, scale, c, n2, false, kf);
+  if constexpr (SR) c = sr_block_codes(u, kf, scale, sg, c, sr_key, (uint64_t)e0);
+  *reinterpret_cast<uint2*>(codes + e0 / 2) = make_uint2((uint32_t)c, (uint32_t)(c >> 32));
+  scales[blk] = (uint8_t)scale;
+}
+
+hipError_t launch_mom_encode(const float* g, uint8_t* codes, uint8_t* scales, int64_t n, bool has_prev,
+                             uint32_t prev_mask, uint32_t mask, bool rotate, bool adaptive, bool sr, float b1,
+                             float b2, MatScalars* sc, float* tensor_scale, uint64_t sr_key, hipStream_t st) {
+  const int64_t nblk = n / 16;
+  const dim3 grid((uint32_t)((nblk + 255) / 256));
+  if (sr)
+    hipLaunchKernelGGL(k_mom_encode<true>, grid, dim3(256), 0, st, g, codes, scales, nblk, (int)has_prev, prev_mask,
+                       mask, (int)rotate, (int)adaptive, b1, b2, sc, tensor_scale, sr_key);
+  else
+    hipLaunchKernelGGL(k_mom_encode<false>, grid, dim3(256), 0, st, g, codes, scales, nblk, (int)has_prev, prev_mask,
+                       mask, (int)rotate, (int)adaptive, b1, b2, sc, tensor_scale, sr_key);
+  return hipGetLastError();
 }
 
 hipError_t launch_mom_update(const float* g, float* m, int64_t batch, int64_t rows, int64_t cols,

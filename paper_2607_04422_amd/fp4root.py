@@ -314,11 +314,12 @@ def fp4root_apply_update(w: torch.Tensor, o: torch.Tensor, lr: float, wd: float,
 class QAdamWState:
     """Both quantized AdamW moments of a flat parameter of n elements (device tensors)."""
 
-    def __init__(self, n: int, device="cuda"):
+    def __init__(self, n: int, device="cuda", keep_m: bool = False):
         if n <= 0 or n % 256:
             raise ValueError("n must be a positive multiple of 256")
         self.n = n
-        self.m = torch.empty(n, dtype=torch.float32, device=device)
+        # this step's binary32 first moment, written only when kept (diagnostics)
+        self.m = torch.empty(n, dtype=torch.float32, device=device) if keep_m else None
         self.m_codes = torch.zeros(n // 2, dtype=torch.uint8, device=device)
         self.m_scales = torch.zeros(n // 16, dtype=torch.uint8, device=device)
         self.m_tensor_scale = torch.zeros(1, dtype=torch.float32, device=device)

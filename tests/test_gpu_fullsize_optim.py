@@ -59,7 +59,7 @@ def test_qadamw_qo_parameter_full_size():
     rng = np.random.default_rng(5)
     w_np = Q.bf16_round((rng.standard_normal(n) * 0.02).astype(np.float32))
     w = torch.from_numpy(w_np.view(np.int16).copy()).cuda().view(torch.bfloat16)
-    st = F.QAdamWState(n)
+    st = F.QAdamWState(n, keep_m=True)
     m_prev = v_prev = None
     for t in range(2):
         g_np = workloads.matrix(3072, 3072, seed=40 + t).reshape(-1) * np.float32(1e-3)

@@ -37,7 +37,7 @@ def test_qadamw_parity(n, flags):
     lr, wd, b1, b2, eps, seed = 1e-3, 0.1, 0.9, 0.95, 1e-8, 5
     w_np = Q.bf16_round((rng.standard_normal(n) * 0.02).astype(np.float32))
     w = torch.from_numpy(w_np.view(np.int16).copy()).cuda().view(torch.bfloat16)
-    st = F.QAdamWState(n)
+    st = F.QAdamWState(n, keep_m=True)
     m_prev = v_prev = None
     for t in range(3):
         g_np = (rng.standard_t(3, n) * np.repeat(rng.lognormal(0, 1, n // 256), 256) * 1e-3).astype(np.float32)
