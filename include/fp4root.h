@@ -182,9 +182,10 @@ size_t fp4root_momentum_workspace(int64_t batch, int64_t rows, int64_t cols);
  *      magnitude rounds stochastically with the chosen scale r = fl32(s s_g):
  *      with x = |u| / r exact and lo <= x < hi neighbours on the E2M1 grid, it
  *      rounds up to hi iff rho 2^-24 < (x - lo) / (hi - lo) (x >= 6 gives 6,
- *      r = 0 gives 0, the sign bit is kept), rho = SplitMix64 output e + 1 of
- *      state SplitMix64(seed ^ 0x5352, step + 1), shifted right by 40 bits, for
- *      the element at flat index e = (b rows + i) cols + j.
+ *      r = 0 gives 0, the sign bit is kept), rho = 24 bits of SplitMix64 output
+ *      floor(e / 2) + 1 of state SplitMix64(seed ^ 0x5352, step + 1) (bits 40..63
+ *      for even e, 16..39 for odd e), for the element at flat index
+ *      e = (b rows + i) cols + j.
  * Signs d of step t: bit i of SplitMix64 output t + 1 of state `seed` set means
  * d_i = -1 (the rule of the NS steps).
  *   g, m:   device, batch x rows x cols FP32, contiguous (row stride cols, matrix

@@ -24,9 +24,10 @@ The paper fixes none of the arithmetic; the readings taken here:
   rho 2^-24 < (x - lo) / (hi - lo), rho a 24-bit uniform integer; x >= 6 gives
   6; the sign bit is kept; r = 0 gives magnitude 0.  The comparison is exact:
   rho (hi - lo) r < (|u| - lo r) 2^24 holds every term exactly in binary64;
-* draws: rho of the element at flat index e (matrix b, row i, column j:
-  e = (b R + i) C + j) is SplitMix64 output e + 1 of the state
-  SplitMix64(seed XOR 0x5352, t + 1), shifted right by 40 bits.
+* draws: the element at flat index e (matrix b, row i, column j:
+  e = (b R + i) C + j) takes 24 bits of SplitMix64 output floor(e / 2) + 1 of the
+  state SplitMix64(seed XOR 0x5352, t + 1): bits 40..63 for even e, bits 16..39
+  for odd e (one 64-bit output serves two elements).
 """
 from __future__ import annotations
 
@@ -45,19 +46,21 @@ def sr_key(seed: int, step: int) -> int:
 
 
 def sr_draws(key: int, count: int, offset: int = 0) -> np.ndarray:
-    """24-bit draws rho_e = SplitMix64(key, e + 1) >> 40 for e = offset .. offset + count - 1.
+    """24-bit draws for e = offset .. offset + count - 1: z = SplitMix64(key, e // 2 + 1),
+    rho_e = z >> 40 for even e and (z >> 16) & 0xFFFFFF for odd e.
 
     The same three-line SplitMix64 mix as ``rht.splitmix64``, on uint64 arrays
     (NumPy's uint64 arithmetic wraps modulo 2^64).
     """
     e = np.arange(offset, offset + count, dtype=np.uint64)
     with np.errstate(over="ignore"):
-        z = np.uint64(key) + np.uint64(_GAMMA) * (e + np.uint64(1))
+        z = np.uint64(key) + np.uint64(_GAMMA) * (e // np.uint64(2) + np.uint64(1))
         z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
         z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
         z = z ^ (z >> np.uint64(31))
     assert _MASK == (1 << 64) - 1
-    return (z >> np.uint64(40)).astype(np.uint32)
+    odd = (e & np.uint64(1)) == np.uint64(1)
+    return np.where(odd, (z >> np.uint64(16)) & np.uint64(0xFFFFFF), z >> np.uint64(40)).astype(np.uint32)
 
 
 def sr_magnitudes(u: np.ndarray, r: np.ndarray, rho: np.ndarray) -> np.ndarray:

@@ -582,11 +582,14 @@ FP4R_DEV uint64_t sr_block_codes(const float (&u)[16], float kf, uint32_t scale,
   const float r = e4m3_value(scale) * sg;
   if (!(r > 0.0f)) return rtn & 0x8888888888888888ull;   // magnitudes 0, signs kept
   const double rd = (double)r;
-  // SplitMix64 output e0 + i + 1 starts from key + gamma (e0 + 1) + gamma i
-  const uint64_t z0 = key + 0x9E3779B97F4A7C15ull * (e0 + 1);
+  // element e0 + i takes 24 bits of SplitMix64 output (e0 + i) / 2 + 1 (e0 is even):
+  // bits 40..63 for even i, bits 16..39 for odd i
+  const uint64_t z0 = key + 0x9E3779B97F4A7C15ull * (e0 / 2 + 1);
+  uint64_t zk = 0;
   uint64_t out = 0;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
+    if ((i & 1) == 0) zk = splitmix64_mix(z0 + 0x9E3779B97F4A7C15ull * (uint64_t)(i / 2));
     const float ui = kf == 1.0f ? u[i] : u[i] * 0.25f;
     const double a = (double)fabsf(ui);
     const uint32_t c = (uint32_t)(rtn >> (4 * i)) & 15u;
@@ -598,7 +601,7 @@ FP4R_DEV uint64_t sr_block_codes(const float (&u)[16], float kf, uint32_t scale,
     }
     if (idx < 7) {
       const double hi = e2m1_grid(idx + 1);
-      const uint32_t rho = (uint32_t)(splitmix64_mix(z0 + 0x9E3779B97F4A7C15ull * (uint64_t)i) >> 40);
+      const uint32_t rho = (uint32_t)(zk >> ((i & 1) ? 16 : 40)) & 0xFFFFFFu;
       if ((double)rho * (hi - lo) * rd < (a - lo * rd) * 16777216.0) ++idx;
     }
     out |= (uint64_t)((c & 8u) | idx) << (4 * i);

@@ -27,7 +27,7 @@ from paper_2607_04422_amd import workloads
 def test_sr_draws_match_scalar_generator():
     for key, off in [(0, 0), (0x123456789ABCDEF, 5), (M.sr_key(7, 3), (1 << 33) - 10)]:
         d = M.sr_draws(key, 40, off)
-        want = [rht.splitmix64(key, e + 1) >> 40 for e in range(off, off + 40)]
+        want = [(rht.splitmix64(key, e // 2 + 1) >> (16 if e % 2 else 40)) & 0xFFFFFF for e in range(off, off + 40)]
         assert d.tolist() == want
         assert d.max() < (1 << 24)
 
