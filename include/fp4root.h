@@ -277,7 +277,7 @@ size_t fp4root_qadamw_workspace(int64_t n);
  *      bc_i = fl32(1 - beta_i^(step+1)) (the power by repeated binary64
  *      multiplication), IEEE division and square root.
  *   w: device BF16 bit patterns [n] (in place); g: device FP32 [n]; m: device FP32
- *   [n] (receives m_t) or NULL; m_codes [n/2], m_scales [n/16], m_tensor_scale [1]: the
+ *   [n] (receives m_t) or NULL, never g (the second pass reads g again); m_codes [n/2], m_scales [n/16], m_tensor_scale [1]: the
  *   first-moment state; v_codes [n/2], v_scales [n/16] (BF16), v_means [n/256]
  *   (BF16): the second-moment state; states are read (step > 0) and overwritten.
  *   All device buffers 16-byte aligned except the state arrays (8-byte codes).

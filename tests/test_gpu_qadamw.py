@@ -70,3 +70,7 @@ def test_qadamw_errors():
         F.QAdamWState(300)
     with pytest.raises(F.Fp4RootError):
         F.fp4root_qadamw_update(w, torch.ones(n, device="cuda"), st, 0, 1e-3, beta2=2.0)
+    g1 = torch.ones(n, device="cuda")
+    st.m = g1                                   # m may not alias g: rejected before any launch
+    with pytest.raises(F.Fp4RootError):
+        F.fp4root_qadamw_update(w, g1, st, 0, 1e-3)
