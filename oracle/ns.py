@@ -13,9 +13,10 @@ Readings taken where the paper is silent:
 * the first line's X is X_k;
 * tall matrices (rows > cols) are transposed so that the Gram matrix is the
   short side's (m = min(rows, cols) square);
-* X_k, A_k and B_k are binary32 between products; each product is evaluated in
-  binary64 from the exact decoded operands and rounded once to binary32 (B_k
-  after its binary64 combination with b A_k);
+* X_k, A_k and B_k are binary32 between products; each product's sums are
+  exact, rounded once to binary64 (``block_dot64``), then combined in binary64
+  as the formulas read and rounded once to binary32 (B_k after its binary64
+  combination with b A_k);
 * A_k is exactly symmetric, so qA_k^16x1 is qA_k transposed bit for bit and
   B_k's product is the Gram matrix of qA_k;
 * before the iteration the momentum is clipped at its p99 magnitude and
@@ -24,8 +25,12 @@ Readings taken where the paper is silent:
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 from scipy.linalg.blas import dsyrk
+
+from .formats import E2M1_GRID
 
 from .quantile import clip, clip_threshold
 from .quantize import quantize
@@ -41,6 +46,71 @@ def gram64(d: np.ndarray) -> np.ndarray:
         return np.zeros((0, 0))
     u = dsyrk(1.0, d, lower=0)
     return np.triu(u) + np.triu(u, 1).T
+
+
+def _integer_rows(q):
+    """Decoded NVFP4 values of every row as (I, e): value = I * 2^(e - 11) per element.
+
+    q * s with q = k / 2 (|k| <= 12) and the E4M3 scale s = M 2^(e - 10) (normal:
+    M = 8 + mantissa, e = the exponent field; subnormal: M = mantissa, e = 1), so
+    I = k M is an integer with |I| <= 180.  Returns I (float64, exact) and e per
+    element (int64), plus each row's largest e over its non-zero elements.
+    """
+    codes = np.asarray(q.codes)
+    sc = np.asarray(q.scales).astype(np.int64)
+    rows, cols = codes.shape
+    k = np.rint(E2M1_GRID[codes & 7] * 2.0)
+    k = np.where(codes & 8, -k, k)
+    ef = (sc >> 3) & 15
+    mant = sc & 7
+    M = np.where(ef == 0, mant, 8 + mant).astype(np.float64)
+    e = np.where(ef == 0, 1, ef)
+    I = (k.reshape(rows, cols // 16, 16) * M[..., None]).reshape(rows, cols)
+    E = np.repeat(e, 16, axis=1)
+    emax = np.where(I != 0, E, -1).max(axis=1) if cols else np.full(rows, -1)
+    return I, E, emax
+
+
+def block_dot64(qa, qb=None) -> np.ndarray:
+    """binary64 rounding of the exact sums  sum_k D(qa)_ik D(qb)_jk  (D = q * s, no
+    tensor scale) for every i, j; qb = None gives the Gram matrix of qa, exactly symmetric.
+
+    Each row is scaled by 2^(-its largest exponent), which leaves integers times powers of
+    two no smaller than 2^-(spread); a binary64 BLAS product of such rows is exact in any
+    summation order whenever every partial sum fits 53 bits, i.e. when
+    K * 180^2 * 2^(spread_a(i) + spread_b(j)) < 2^53.  Entries whose rows fail that
+    condition are summed with math.fsum, which is correctly rounded.
+    """
+    Ia, Ea, ma = _integer_rows(qa)
+    if qb is None:
+        Ib, Eb, mb = Ia, Ea, ma
+    else:
+        Ib, Eb, mb = _integer_rows(qb)
+    K = Ia.shape[1]
+    if K == 0 or Ia.shape[0] == 0 or Ib.shape[0] == 0:
+        return np.zeros((Ia.shape[0], Ib.shape[0]))
+    sa = np.where(Ia != 0, np.ldexp(1.0, Ea - np.maximum(ma, 0)[:, None]), 0.0)
+    sb = np.where(Ib != 0, np.ldexp(1.0, Eb - np.maximum(mb, 0)[:, None]), 0.0)
+    ta, tb = Ia * sa, Ib * sb                     # exact: |I| <= 180 times a power of two
+    if qb is None:
+        u = dsyrk(1.0, ta, lower=0)
+        d = np.triu(u) + np.triu(u, 1).T
+    else:
+        d = ta @ tb.T
+    # spread of each row: its largest minus its smallest exponent over non-zero elements
+    spa = ma - np.where(Ia != 0, Ea, 99).min(axis=1)
+    spb = mb - np.where(Ib != 0, Eb, 99).min(axis=1)
+    spa = np.where(ma < 0, 0, spa)
+    spb = np.where(mb < 0, 0, spb)
+    bits = np.log2(K * 180.0 * 180.0) + spa[:, None] + spb[None, :]
+    out = np.ldexp(d, (np.maximum(ma, 0)[:, None] + np.maximum(mb, 0)[None, :]) - 22)
+    bad = np.argwhere(bits >= 53.0)
+    if len(bad):
+        va = Ia * np.ldexp(1.0, Ea - 11)
+        vb = Ib * np.ldexp(1.0, Eb - 11)
+        for i, j in bad:
+            out[i, j] = math.fsum(va[i] * vb[j])   # each product exact (at most 16 bits)
+    return out
 
 
 def f32(x) -> np.ndarray:
@@ -61,13 +131,12 @@ def ns_step_nvfp4(x, a, b, c, signs=None, adaptive46=True, trace=None):
     a64, b64, c64 = (np.float64(np.float32(t)) for t in (a, b, c))
     qx = quantize(x, 1, signs, adaptive46)
     qxt = quantize(x, 0, signs, adaptive46)
-    A = f32((np.float64(qx.sg) * np.float64(qx.sg)) * gram64(qx.block_values()))
+    A = f32((np.float64(qx.sg) * np.float64(qx.sg)) * block_dot64(qx))
     qa = quantize(A, 1, signs, adaptive46)
-    da = qa.block_values()
-    P = (np.float64(qa.sg) * np.float64(qa.sg)) * gram64(da)
+    P = (np.float64(qa.sg) * np.float64(qa.sg)) * block_dot64(qa)
     B = f32(b64 * A.astype(np.float64) + c64 * P)
     qb = quantize(B, 1, signs, adaptive46)
-    prod = qb.block_values() @ qxt.block_values().T
+    prod = block_dot64(qb, qxt)
     x1 = f32(a64 * x.astype(np.float64) + (np.float64(qb.sg) * np.float64(qxt.sg)) * prod)
     if trace is not None:
         trace.update(qx=qx, qxt=qxt, A=A, qa=qa, B=B, qb=qb)
