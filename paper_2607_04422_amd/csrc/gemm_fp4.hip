@@ -13,7 +13,9 @@
 // |sum| < 2^19 of those units, so the MFMA result (accumulator input 0) is the
 // exact block sum.  Block sums are accumulated in binary64 and the epilogue
 // forms the output in binary64 and rounds once to binary32, so every product
-// equals the binary32 rounding of its exact value.
+// equals the binary32 rounding of its exact value whenever the binary64 running
+// sums are exact (every partial sum within 53 bits of the smallest product unit,
+// which holds unless the block exponents of a row span more than about 20 binades).
 //
 // Chained blocks.  Element values are q s with q = k/2 (|k| <= 12) and
 // s = M 2^(e-10) (E4M3: M <= 15, e >= 1; subnormal scales as M = m, e = 1), so
@@ -25,12 +27,20 @@
 // = sum_b n2_b 4^(e_b - ea_min(i)) (n2 = sum (2q)^2 M^2 per block; sigma_j alike)
 // the bound is below 2^24 u whenever rho_i sigma_j < 2^48; then every partial
 // sum is exactly representable in binary32, and the MFMAs of the group may
-// accumulate into one binary32 register, folded into binary64 once.  The encoder
-// stores rho per stage (four blocks) and 16 rows, rounded up to binary32, and
-// each compute wave tests the maxima over its own rows (diagonal tiles of
-// symmetric products test tile-wide maxima, so that (i, j) and (j, i) add the
-// same binary32 values in the same order and the product stays exactly
-// symmetric).
+// accumulate into one binary32 register, folded into binary64 once.  The encoders
+// store rho per 16 rows for every 64-element stage (four blocks), rounded up to
+// binary32.  Each compute wave tests the maxima over its own rows (diagonal tiles
+// of symmetric products test tile-wide maxima, so that (i, j) and (j, i) add the
+// same binary32 values in the same order and the product stays exactly symmetric)
+// and runs every stage either as one group or as one group per block.
+//
+// Work per wave: a 32 x 64 output tile (1 x 2 MFMA tiles), 32 binary64
+// accumulators and 32 binary32 chain registers per lane; eight waves share a
+// 128 x 128 workgroup tile and two workgroups a CU (four waves per SIMD).  Per
+// MFMA the exact path issues 8 fold instructions (one conversion and one binary64
+// add per output and stage) and 4 decode instructions; per stage a wave waits for
+// its LDS operand reads, for the staged loads of the next stage and at the
+// barrier, which the other waves of its SIMD cover only in part.
 #include "device.h"
 #include "internal.h"
 
@@ -40,7 +50,6 @@ namespace fp4r {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Tile configuration of the exact NVFP4 product: WAVES_M x WAVES_N waves, each
@@ -58,30 +67,28 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #ifndef FP4R_FP4_TN
 #define FP4R_FP4_TN 2
 #endif
-constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
-// Chained accumulation of block groups whose exactness bound holds (1) or one
-// binary64 fold per block (0).
-#ifndef FP4R_FP4_CHAIN
-#define FP4R_FP4_CHAIN 1
+#ifndef FP4R_FP4_WAVES_PER_EU
+#define FP4R_FP4_WAVES_PER_EU 4
 #endif
+constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
 
-// LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two 16-byte
-// halves h) of row r at byte
-//   kb_base(kb) + 32 r + 16 (h ^ bit 2 of r),   kb_base(kb) = 32 ROWS kb + {0, 64, 144, 208}[kb].
-// A 16-byte access is served per 8 lanes.  MFMA operand reads (8 consecutive rows,
-// one block and half) then cover all 32 banks, and so do the loader's writes
-// (rows r, r + 1 times the four blocks: the block bases differ by 0, 64, 16 and 80
-// modulo 128 bytes).  The block and buffer offsets are constants, so one address
-// register per operand tile serves every block of both buffers.
-FP4R_DEV int lds_row_off(int row, int h) { return row * 32 + ((h ^ ((row >> 2) & 1)) << 4); }
+// LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two
+// 16-byte halves h) of row r at byte
+//   base(kb) + 32 r + 16 (h ^ sw(r)),   base(kb) = 32 ROWS kb + {0, 128, 272, 400}[kb],
+// sw(r) = bit 2 of r xor bit 3 of r.  A 16-byte LDS access is served 16 lanes per
+// cycle over 64 banks (256 bytes).  The MFMA operand reads (16 consecutive rows of
+// one block and half per 16 lanes) then fall in distinct banks through the swizzle,
+// and so do the loader's writes (4 rows x the 4 blocks per 16 lanes) through the
+// block offsets, which are 0, 8, 1 and 9 sixteen-byte units modulo 256 bytes.  The
+// offsets are constants, so one address register per operand tile serves every
+// block of both buffers.
+FP4R_DEV int lds_row_off(int row, int h) { return row * 32 + ((h ^ ((row >> 2) & 1) ^ ((row >> 3) & 1)) << 4); }
 template <int ROWS>
-constexpr int lds_kb_base(int kb) {
-  return 32 * ROWS * kb + (kb == 0 ? 0 : kb == 1 ? 64 : kb == 2 ? 144 : 208);
-}
+__host__ __device__ constexpr int lds_kb_base(int kb) { return 32 * ROWS * kb + 128 * kb + 16 * (kb >> 1); }
 template <int ROWS>
 constexpr int lds_stage_bytes() { return lds_kb_base<ROWS>(3) + 32 * ROWS; }
-static_assert(lds_kb_base<128>(2) == 32 * 128 * 2 + 64 * 2 + 16 && lds_kb_base<128>(3) == 32 * 128 * 3 + 64 * 3 + 16,
-              "block bases");
+static_assert(lds_kb_base<128>(0) == 0 && lds_kb_base<128>(1) % 256 == 128 && lds_kb_base<128>(2) % 256 == 16 && lds_kb_base<128>(3) % 256 == 144,
+              "block offsets");
 
 // Output tile coordinates.  Symmetric products enumerate the upper triangle
 // row by row; others are row-major over (tiles_m x tiles_n).
@@ -103,21 +110,23 @@ FP4R_DEV void tile_coords(int64_t t, int tiles_m, int tiles_n, bool sym, int& tm
 
 // ---------------------------------------------------------------------------
 // NVFP4 operand staging: each thread loads whole 16-element blocks (8 code
-// bytes + 1 scale byte), decodes them to f16 and writes them to LDS.
+// bytes + 1 scale byte), decodes them to f16 and writes them to LDS.  Block
+// slot idx = thread + NT j (j < kPer) stages row idx / 4, block idx % 4 of the
+// stage: four consecutive lanes read 32 contiguous bytes of codes.
 
 template <int ROWS, int NT>
 struct Fp4Stage {
   static constexpr int kPer = ROWS * 4 / NT;   // blocks per thread per stage
-  static_assert(kPer == 1, "each thread stages one block of each operand per stage");
+  static_assert(kPer >= 1 && ROWS * 4 == kPer * NT, "whole blocks per thread");
   uint2 codes[kPer];
   uint32_t scales[kPer];
 };
 
-// Where a thread's blocks come from: raw buffer resources over the tile's rows
-// of codes and scales (the hardware range check returns 0 for rows past the
-// matrix, so the tail tile needs no branch).  Thread t stages row t / 4, block
-// t % 4 of every 64-element stage: scale byte (t / 4) nkb + t % 4 + 4 s and the
-// codes at eight times that offset, the same offsets for both operands.
+FP4R_DEV int stage_row(int idx) { return idx >> 2; }
+FP4R_DEV int stage_kb(int idx) { return idx & 3; }
+
+// Raw buffer resources over the tile's rows of codes and scales (the hardware
+// range check returns 0 for rows past the matrix, so the tail tile needs no branch).
 constexpr int kBufWord3 = 0x00020000;          // raw 32-bit data format, no swizzle
 constexpr uint32_t kBufOutOfRange = 0x7FFFFFF0u;
 
@@ -139,16 +148,19 @@ FP4R_DEV Fp4Src fp4_src(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t
 
 template <int ROWS, int NT>
 FP4R_DEV void fp4_load(const Fp4Src& src, int nkb, int stage, Fp4Stage<ROWS, NT>& s) {
-  // blocks past the end of K read as 0 (nkb < 2^17; the block index is recomputed
-  // from the thread index, which is cheaper than keeping it live)
-  const int kq = (int)(threadIdx.x & 3);
-  const bool valid = stage * 4 + kq < nkb;
-  const uint32_t o = (threadIdx.x >> 2) * (uint32_t)nkb + (uint32_t)(kq + 4 * stage);
-  const uint32_t oc = valid ? 8u * o : kBufOutOfRange;
-  const uint32_t os = valid ? o : kBufOutOfRange;
-  const auto c = __builtin_amdgcn_raw_buffer_load_b64(src.codes, (int)oc, 0, 0);
-  s.codes[0] = make_uint2(c[0], c[1]);
-  s.scales[0] = __builtin_amdgcn_raw_buffer_load_b8(src.scales, (int)os, 0, 0);
+  // blocks past the end of K read as 0 (nkb < 2^17)
+#pragma unroll
+  for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
+    const int idx = (int)threadIdx.x + NT * j;
+    const int kq = stage_kb(idx);
+    const bool valid = stage * 4 + kq < nkb;
+    const uint32_t o = (uint32_t)stage_row(idx) * (uint32_t)nkb + (uint32_t)(kq + 4 * stage);
+    const uint32_t oc = valid ? 8u * o : kBufOutOfRange;
+    const uint32_t os = valid ? o : kBufOutOfRange;
+    const auto c = __builtin_amdgcn_raw_buffer_load_b64(src.codes, (int)oc, 0, 0);
+    s.codes[j] = make_uint2(c[0], c[1]);
+    s.scales[j] = __builtin_amdgcn_raw_buffer_load_b8(src.scales, (int)os, 0, 0);
+  }
 }
 
 template <int SEL>
@@ -158,34 +170,13 @@ FP4R_DEV f16x2 fp4_pair(uint32_t w, f16x2 s2) {
   return q * s2;
 }
 
-// Chain records of one operand: the encoder stores, per 64-element stage and 16
-// rows, the largest rho (see the header), [K/64][rows/16].  Two ways to bring
-// them to a compute wave (chosen per product by measurement):
-// * table: before the stage loop each wave evaluates rho sigma over its own row
-//   groups for every stage (one stage per lane) into its column of an LDS table,
-//   so the loop reads one value per stage (K up to 64 kRecStages);
-// * scalar: per stage the wave reads its groups' records through the constant
-//   address space (written by an earlier kernel, never by this one), so the
-//   wave-uniform loads become scalar loads, one stage ahead.
-constexpr int kRecStages = 256;   // table: longer K (over 16384) folds every block
-typedef const float __attribute__((address_space(4))) cfloat;
-
-// Largest record of groups [g0, g0 + n) of stage s, clamped to the operand's
-// groups (a tail tile's missing rows are zero and need no record).
-FP4R_DEV float rho_records_max(const float* rec, int64_t ngroups, int s, int g0, int n) {
-  cfloat* p = (cfloat*)(rec + (int64_t)s * ngroups);
-  float m = 0.0f;
-  for (int g = 0; g < n; ++g) m = fmaxf(m, p[min((int64_t)(g0 + g), ngroups - 1)]);
-  return m;
-}
-
 // Decodes the staged blocks into the LDS stage at `lds`.
 template <int ROWS, int NT>
 FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
 #pragma unroll
   for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
-    const int idx = threadIdx.x + NT * j;
-    const int r = idx >> 2, kb = idx & 3;
+    const int idx = (int)threadIdx.x + NT * j;
+    const int r = stage_row(idx), kb = stage_kb(idx);
     // the E4M3 scale in both halves, converted exactly (every E4M3 value is an f16)
     const f16x2 s2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8((s.scales[j] & 0xFFu) * 0x0101u, 1.0f, false);
     const uint32_t w[2] = {s.codes[j].x, s.codes[j].y};
@@ -196,11 +187,20 @@ FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
       f16x8 v;
       v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
-      const int kbo = 32 * ROWS * kb + 64 * kb + 16 * (kb >> 1);   // lds_kb_base<ROWS>(kb)
-      *reinterpret_cast<f16x8*>(lds + kbo + lds_row_off(r, half)) = v;
+      *reinterpret_cast<f16x8*>(lds + lds_kb_base<ROWS>(kb) + lds_row_off(r, half)) = v;
     }
+    // one block at a time: few temporaries while the chain registers of a stage
+    // pair are live
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
+
+// Chain records of one operand (see the header): per 64-element stage and 16 rows,
+// [K/64][rows/16], and per stage pair, [K/128][rows/16].  Before the stage loop
+// each wave evaluates rho sigma over its own row groups for every stage (up to
+// kRecStages, K = 32768) into its column of an LDS byte table; the loop reads one
+// byte per stage.
+constexpr int kRecStages = 512;
 
 // ---------------------------------------------------------------------------
 // Rotated amaxes of an output, for the tensor scale of the operand encoded from
@@ -296,14 +296,16 @@ FP4R_DEV uint32_t wave_max_bits(float v) {
 // ---------------------------------------------------------------------------
 // Exact NVFP4 product.
 
-#ifndef FP4R_FP4_WAVES_PER_EU
-#define FP4R_FP4_WAVES_PER_EU 4
-#endif
+// Accumulation form of one stage (uniform over a wave): one group per block, or
+// the stage as one group.
+enum StageForm { kFormBlock = 0, kFormStage = 1 };
+template <int F>
+using form_t = std::integral_constant<int, F>;
 
 template <int MODE, int WM_, int WN_, int TM, int TN>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) {
-  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
+  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64, NW = WM_ * WN_;
   // padded row of the FP32 output tile staged in LDS: rows stay 16-byte aligned, and
   // the two half-waves of an MFMA-layout write (rows 4 apart) fall 32 banks apart
   constexpr int kLdT = BN + 8;
@@ -312,17 +314,19 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   constexpr size_t kEpiBytes = (size_t)BM * kLdT * sizeof(float);
   constexpr int kGa = BM / 16, kGb = BN / 16;   // 16-row groups per operand tile
   __shared__ __attribute__((aligned(16))) char smem[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
-  constexpr bool kTable = MODE != kModeUpdateX;   // record delivery (see above)
-  __shared__ uint8_t wflags[FP4R_FP4_CHAIN && kTable ? kRecStages : 1][NT / 64];
-  __shared__ uint32_t red[2][NT / 64];   // per-wave amaxes (rows, columns)
-  char(*lds_a)[kStA] = reinterpret_cast<char(*)[kStA]>(smem);
-  char(*lds_b)[kStB] = reinterpret_cast<char(*)[kStB]>(smem + 2 * kStA);
+  __shared__ uint8_t wflags[kRecStages][NW];
+  __shared__ uint32_t red[2][NW];   // per-wave amaxes (rows, columns)
+  char* const la0 = smem;
+  char* const la1 = smem + kStA;
+  char* const lb0 = smem + 2 * kStA;
+  char* const lb1 = smem + 2 * kStA + kStB;
   constexpr bool kSym = MODE != kModeUpdateX;
   const int64_t mat = blockIdx.x / tiles_per_mat;
   int tm, tn;
   tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int wm = wave / WN_, wn = wave % WN_;
   const int nkb = (int)(g.K / 16);   // K <= 2^21
   const int nstages = (int)((nkb + 3) / 4);
@@ -337,22 +341,18 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
 
   const Fp4Src src_a = fp4_src<BM>(g.a, mat, g.M, g.K, row0);
   const Fp4Src src_b = fp4_src<BN>(g.b, mat, g.N, g.K, col0);
+
   // a group chains if rho sigma < 2^48; the limit leaves room for the rounding of
   // the binary32 product rho * sigma
-  constexpr float kLimStage = 281474976710656.0f * (1.0f - 1.0f / 65536.0f);   // 2^48 (1 - 2^-16)
-#if FP4R_FP4_CHAIN
-  static_assert(kGa == kGb, "square tiles");
-  // the rows a compute wave covers: TM * 2 loader groups of A, TN * 2 of B;
-  // diagonal tiles of symmetric products use all groups (see the header)
-  const int uwave = __builtin_amdgcn_readfirstlane(wave);
+  constexpr float kLim = 281474976710656.0f * (1.0f - 1.0f / 65536.0f);   // 2^48 (1 - 2^-16)
+  // the rows a compute wave covers: TM * 2 groups of A, TN * 2 of B; diagonal
+  // tiles of symmetric products use all groups of the tile (see the header)
   const bool diag = kSym && tm == tn;
-  const bool chain_on = g.a.rhog != nullptr && g.b.rhog != nullptr && (!kTable || nstages <= kRecStages);
-  const int ga0 = diag ? 0 : (uwave / WN_) * TM * 2, nga = diag ? kGa : TM * 2;
-  const int gb0 = diag ? 0 : (uwave % WN_) * TN * 2, ngb = diag ? kGb : TN * 2;
+  const bool chain_on = g.a.rhog != nullptr && g.b.rhog != nullptr;
+  const int ga0 = diag ? 0 : wm * TM * 2, nga = diag ? kGa : TM * 2;
+  const int gb0 = diag ? 0 : wn * TN * 2, ngb = diag ? kGb : TN * 2;
   const float* rec_a = chain_on ? g.a.rhog + mat * g.a.rhog_bstride : nullptr;
   const float* rec_b = chain_on ? g.b.rhog + mat * g.b.rhog_bstride : nullptr;
-  const float* rec8_a = chain_on && g.a.rho8 ? g.a.rho8 + mat * g.a.rho8_bstride : nullptr;
-  const float* rec8_b = chain_on && g.b.rho8 ? g.b.rho8 + mat * g.b.rho8_bstride : nullptr;
   // the largest record over groups g0 .. g0 + ng - 1 of record row `idx`
   // (missing groups of a tail tile read 0: their rows are zero)
   auto group_max = [&](const float* rec, int64_t groups_all, int64_t idx, int64_t g0, int ng) {
@@ -361,62 +361,47 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
       if (g0 + k < groups_all) mx = fmaxf(mx, rec[idx * groups_all + g0 + k]);
     return mx;
   };
-  // chain flags of stages s0 .. s0 + kRecStages - 1 for this wave's rows into
-  // wflags[.][wave] (one stage per lane): bit 0 = the stage chains, bit 1 (even
-  // stages) = the stage and the next chain as one group.  Only this wave touches
-  // its column, so no barrier is needed.
-  auto fill_flags = [&](int s0) {
-    if (!kTable) return;
+  // chain flags of every stage for this wave's rows into wflags[.][wave] (one
+  // stage per lane and pass): bit 0 = the stage chains.  Only this wave touches its column, so no
+  // barrier is needed.  Stages past kRecStages (K over 64 kRecStages) fold every block.
+  auto fill_flags = [&]() {
     const int64_t nga_all = g.M / 16, ngb_all = g.N / 16;
     const int64_t a0 = row0 / 16 + ga0, b0 = col0 / 16 + gb0;
-#pragma unroll
-    for (int h = 0; h < kRecStages / 64; ++h) {
-      const int ss = lane + 64 * h;
-      const int64_t sg = (int64_t)s0 + ss;
+    const int nfill = nstages < kRecStages ? nstages : kRecStages;
+    for (int s0 = 0; s0 < nfill; s0 += 64) {
+      const int ss = s0 + lane;
       uint32_t f = 0;
-      if (chain_on && sg < nstages) {
-        if (group_max(rec_a, nga_all, sg, a0, nga) * group_max(rec_b, ngb_all, sg, b0, ngb) < kLimStage) f |= 1u;
-        if (rec8_a && rec8_b && (sg & 1) == 0 && sg + 1 < nstages &&
-            group_max(rec8_a, nga_all, sg / 2, a0, nga) * group_max(rec8_b, ngb_all, sg / 2, b0, ngb) < kLimStage)
-          f |= 2u;
+      if (chain_on && ss < nfill) {
+        if (group_max(rec_a, nga_all, ss, a0, nga) * group_max(rec_b, ngb_all, ss, b0, ngb) < kLim) f |= 1u;
       }
-      wflags[ss][wave] = (uint8_t)f;
+      if (ss < kRecStages) wflags[ss][wave] = (uint8_t)f;
     }
   };
-  auto stage_flags = [&](int s) { return (uint32_t)wflags[s % kRecStages][wave]; };
-  auto stage_bound = [&](int s) {
-    if (!chain_on || s >= nstages) return __builtin_inff();
-    return rho_records_max(rec_a, g.M / 16, s, (int)(row0 / 16) + ga0, nga) *
-           rho_records_max(rec_b, g.N / 16, s, (int)(col0 / 16) + gb0, ngb);
-  };
-#endif
+  auto stage_flags = [&](int s) { return s < kRecStages ? (uint32_t)wflags[s][wave] : 0u; };
 
-  // stage -> LDS buffer `buf` (decoded operands)
-  // The decode into LDS runs at raised wave priority: a wave that has finished its
-  // MFMAs then gets the issue slots ahead of waves still in their MFMA or fold phase,
-  // and reaches the barrier sooner (measured: update product -1 to -2 %, Gram of qX
-  // -0.3 to -1.4 %; the Gram of qA, with its short K, lost 2 % and keeps the default).
-  auto put = [&](int buf, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) {
+  // stage -> LDS buffers (decoded operands)
+  // The decode runs at raised wave priority: a wave that has finished its MFMAs
+  // then gets the issue slots ahead of waves still in their MFMA or fold phase, and
+  // reaches the barrier sooner (the Gram of qA, with its short K, keeps the default).
+  auto put = [&](char* la, char* lb, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) __attribute__((always_inline)) {
     if constexpr (MODE != kModeGramB) __builtin_amdgcn_s_setprio(1);
-    fp4_store<BM, NT>(lds_a[buf], xa);
-    fp4_store<BN, NT>(lds_b[buf], xb);
+    fp4_store<BM, NT>(la, xa);
+    fp4_store<BN, NT>(lb, xb);
     if constexpr (MODE != kModeGramB) __builtin_amdgcn_s_setprio(0);
   };
 
   const f32x16 zero = {};
   f32x16 p[TM][TN];   // the binary32 chain registers
-  // MFMAs and binary64 folds of the stage in LDS buffer `buf` (kbs blocks).  fl:
-  // bit k - 1 set = block k accumulates onto block k - 1 (blocks past the end of K
-  // are zero in LDS and join any group).  Odd stages (odd_tag true) start on the
-  // chain registers as left by the previous stage; fold_end folds the registers
-  // at the end, and even stages then clear them for the odd stage after them.
-  auto compute = [&](auto odd_tag, int buf, int kbs, uint32_t fl, bool fold_end) {
-    constexpr bool ODD = decltype(odd_tag)::value;
-    if (kbs <= 0) return;
-    const char* la = lds_a[buf];
-    const char* lb = lds_b[buf];
-#if FP4R_FP4_CHAIN
-    // the TM x TN tiles' chains run interleaved, block by block
+  auto fold = [&](int i, int j) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
+  };
+  // MFMAs of the stage in (la, lb).  A group starts with accumulator input 0 and
+  // is folded into binary64 as soon as it ends (after its last block, or at the end
+  // of the stage), so the chain registers are dead while the next stage decodes.
+  // Blocks past the end of K are zero in LDS and join any group.
+  auto compute = [&](auto form_tag, const char* la, const char* lb) __attribute__((always_inline)) {
+    constexpr int F = decltype(form_tag)::value;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       f16x8 av[TM], bv[TN];
@@ -428,105 +413,71 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
       for (int j = 0; j < TN; ++j)
         bv[j] = *reinterpret_cast<const f16x8*>(
             lb + lds_kb_base<BN>(kb) + lds_row_off((wn * TN + j) * 32 + (lane & 31), lane >> 5));
-      const bool chained = kb > 0 ? ((fl >> (kb - 1)) & 1u) != 0 : ODD;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          if (kb > 0 && !chained) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
-          }
-          p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], chained ? p[i][j] : zero, 0, 0, 0);
+          const bool fresh = F == kFormBlock || kb == 0;
+          p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], fresh ? zero : p[i][j], 0, 0, 0);
         }
       __builtin_amdgcn_sched_barrier(0);   // keep operand loads next to their use
+      if (F == kFormBlock && kb < 3) {
+        // every block a group of its own (rare: the stage bound failed)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) fold(i, j);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    if (fold_end) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[i][j][e];
-          if (!ODD) p[i][j] = zero;
-        }
-    }
-#else
-    (void)fl; (void)fold_end;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      if (kb >= kbs) break;
-      f16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const f16x8*>(
-            la + lds_kb_base<BM>(kb) + lds_row_off((wm * TM + i) * 32 + (lane & 31), lane >> 5));
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const f16x8*>(
-            lb + lds_kb_base<BN>(kb) + lds_row_off((wn * TN + j) * 32 + (lane & 31), lane >> 5));
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bfr[j], zero, 0, 0, 0);
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + (double)p[e];
-        }
-    }
-#endif
+      for (int j = 0; j < TN; ++j) fold(i, j);
   };
-  auto blocks_in = [&](int s) { return nkb - s * 4 < 4 ? nkb - s * 4 : 4; };
+  // one stage that is a group of its own (form Stage) or folds every block (Block)
+  auto run_single = [&](uint32_t f, const char* la, const char* lb) __attribute__((always_inline)) {
+    if (f & 1u) compute(form_t<kFormStage>(), la, lb);
+    else compute(form_t<kFormBlock>(), la, lb);
+  };
 
   Fp4Stage<BM, NT> sa;
   Fp4Stage<BN, NT> sb;
   fp4_load<BM, NT>(src_a, nkb, 0, sa);
   fp4_load<BN, NT>(src_b, nkb, 0, sb);
-  put(0, sa, sb);
-  if (FP4R_FP4_CHAIN) fill_flags(0);
+  put(la0, lb0, sa, sb);
+  // stage 1 loads while the flags are computed (reads 0 past the last stage)
+  fp4_load<BM, NT>(src_a, nkb, 1, sa);
+  fp4_load<BN, NT>(src_b, nkb, 1, sb);
+  fill_flags();
   __syncthreads();
-  // Stage s is computed from LDS buffer s % 2 while stage s + 1 loads into
-  // registers; it is decoded into the other buffer after the MFMAs.
-  if (kTable) {
-    // two stages per iteration, buffers as constants; a stage pair may chain as
-    // one group of eight blocks (one fold per 128 elements); the last stage loads
-    // and decodes nothing
-    for (int s = 0; s < nstages; s += 2) {
-      const uint32_t f0 = FP4R_FP4_CHAIN ? stage_flags(s) : 0u;
-      const bool pair = (f0 & 2u) != 0, has_odd = s + 1 < nstages;
-      if (has_odd) {
-        fp4_load<BM, NT>(src_a, nkb, s + 1, sa);
-        fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-      }
-      compute(std::false_type(), 0, blocks_in(s), (pair || (f0 & 1u)) ? 7u : 0u, !pair);
-      if (has_odd) put(1, sa, sb);
-      __syncthreads();
-      if (!has_odd) break;
-      const uint32_t f1 = FP4R_FP4_CHAIN ? stage_flags(s + 1) : 0u;
-      const bool more = s + 2 < nstages;
-      if (more) {
-        fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
-        fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
-      }
-      compute(std::true_type(), 1, blocks_in(s + 1), (pair || (f1 & 1u)) ? 7u : 0u, true);
-      if (more) put(0, sa, sb);
-      __syncthreads();
+  // Two stages per iteration with the LDS buffers as constants: stage s computes
+  // from one buffer while stage s + 1, loaded during the previous stage, decodes
+  // into the other; the loads of stage s + 2 are issued into the same registers
+  // right after that decode, so they have the barrier and a whole stage of MFMAs
+  // to arrive.  Loads past the last stage read 0 and are never decoded.
+  for (int s = 0; s < nstages; s += 2) {
+    const bool has_odd = s + 1 < nstages, more = s + 2 < nstages;
+    run_single(stage_flags(s), la0, lb0);
+    if (has_odd) {
+      put(la1, lb1, sa, sb);
+      fp4_load<BM, NT>(src_a, nkb, s + 2, sa);
+      fp4_load<BN, NT>(src_b, nkb, s + 2, sb);
     }
-  } else {
-    float st = FP4R_FP4_CHAIN ? stage_bound(0) : 0.0f;
-    // (unconditional loads and stores past the last stage: measured faster here)
-    for (int s = 0; s < nstages; ++s) {
-      fp4_load<BM, NT>(src_a, nkb, s + 1, sa);   // reads 0 past the last stage
-      fp4_load<BN, NT>(src_b, nkb, s + 1, sb);
-      compute(std::false_type(), s & 1, blocks_in(s), st < kLimStage ? 7u : 0u, true);
-      put((s & 1) ^ 1, sa, sb);
-      if (FP4R_FP4_CHAIN) st = stage_bound(s + 1);
-      __syncthreads();
+    __syncthreads();
+    if (!has_odd) break;
+    run_single(stage_flags(s + 1), la1, lb1);
+    if (more) {
+      put(la0, lb0, sa, sb);
+      fp4_load<BM, NT>(src_a, nkb, s + 3, sa);
+      fp4_load<BN, NT>(src_b, nkb, s + 3, sb);
     }
+    __syncthreads();
   }
 
   // epilogue: binary64 formula, one rounding to binary32, staged through LDS
-  // (the main loop's buffers are free after the last barrier)
+  // (the main loop's buffers are free after its last barrier), one MFMA tile at
+  // a time
   const double sga = (double)g.sc[mat].sg[g.slot_a], sgb = (double)g.sc[mat].sg[g.slot_b];
   const double alpha = sga * sgb;   // exact: product of two binary32 values
   const double ca = (double)g.ca, cb = (double)g.cb, cc = (double)g.cc;
@@ -552,23 +503,6 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
           xin[i][j][e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)off, 0, 0));
         }
   }
-  // this lane's outputs in binary32 (zero outside the matrix), also staged in LDS
-  float val[TM][TN][16];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int rl = (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int cl = (wn * TN + j) * 32 + (lane & 31);
-        double v = alpha * acc[i][j][e];
-        if (MODE == kModeGramB) v = cb * (double)xin[i][j][e] + cc * v;
-        if (MODE == kModeUpdateX) v = ca * (double)xin[i][j][e] + v;
-        const bool in = row0 + rl < g.M && col0 + cl < g.N;
-        val[i][j][e] = in ? (float)v : 0.0f;
-        tile[rl * kLdT + cl] = val[i][j][e];
-      }
   // off-diagonal tiles of symmetric products (and a transposed final output): the
   // transposed tile straight from registers (four consecutive rows of a column
   // form a row segment of it)
@@ -577,97 +511,79 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   float* const fin_out = fin ? g.fin_out[mat] : nullptr;
   const int64_t fin_ld = fin ? g.fin_ld[mat] : 0;
   const bool fin_tall = fin && g.fin_tall[mat] != 0;
-  if (fin_tall) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int rb = (wm * TM + i) * 32 + 8 * e4 + 4 * (lane >> 5);
-          const int cl = (wn * TN + j) * 32 + (lane & 31);
-          const int64_t ur = col0 + cl, uc = row0 + rb;
-          if (ur < g.N && uc < g.M)
-            *reinterpret_cast<float4*>(fin_out + ur * fin_ld + uc) =
-                make_float4(val[i][j][4 * e4], val[i][j][4 * e4 + 1], val[i][j][4 * e4 + 2], val[i][j][4 * e4 + 3]);
-        }
-  }
-  if (mirror) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int rb = (wm * TM + i) * 32 + 8 * e4 + 4 * (lane >> 5);
-          const int cl = (wn * TN + j) * 32 + (lane & 31);
-          const int64_t mr = col0 + cl, mc = row0 + rb;
-          if (mr < g.N && mc < g.M)
-            *reinterpret_cast<float4*>(out + mr * g.N + mc) =
-                make_float4(val[i][j][4 * e4], val[i][j][4 * e4 + 1], val[i][j][4 * e4 + 2], val[i][j][4 * e4 + 3]);
-        }
-  }
-  // rotated amaxes: 16-row blocks of every column (the mirrored tile's rows, or
-  // X_{k+1} along m) from registers, 16-column blocks of every row from LDS
   const bool do_rows = g.amax_row_slot >= 0;
   const bool do_cols = g.amax_col_slot >= 0 && (!kSym || mirror);
   float cmax = 0.0f, rmax = 0.0f;
-  if (do_cols) {
-    if (g.amax_rotate) {
-      const int hb = lane >> 5;
-      float sg[8];
+  const int hb = lane >> 5;
+  float csg[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        sg[e] = ((g.amax_mask >> ((e & 3) + 4 * hb + 8 * (e >> 2))) & 1u) ? -1.0f : 1.0f;
-      const float s4 = hb ? -1.0f : 1.0f;
+  for (int e = 0; e < 8; ++e) csg[e] = ((g.amax_mask >> ((e & 3) + 4 * hb + 8 * (e >> 2))) & 1u) ? -1.0f : 1.0f;
+  const float cs4 = hb ? -1.0f : 1.0f;
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          cmax = fmaxf(cmax, rot_cols_max8<0>(val[i][j], sg, s4));
-          cmax = fmaxf(cmax, rot_cols_max8<8>(val[i][j], sg, s4));
+    for (int j = 0; j < TN; ++j) {
+      // this lane's outputs of MFMA tile (i, j) in binary32 (zero outside the matrix)
+      float val[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int rl = (wm * TM + i) * 32 + 8 * (e >> 2) + 4 * hb + (e & 3);
+        const int cl = (wn * TN + j) * 32 + (lane & 31);
+        double v = alpha * acc[i][j][e];
+        if (MODE == kModeGramB) v = cb * (double)xin[i][j][e] + cc * v;
+        if (MODE == kModeUpdateX) v = ca * (double)xin[i][j][e] + v;
+        const bool in = row0 + rl < g.M && col0 + cl < g.N;
+        val[e] = in ? (float)v : 0.0f;
+        tile[rl * kLdT + cl] = val[e];
+      }
+      const int cl = (wn * TN + j) * 32 + (lane & 31);
+      if (fin_tall || mirror) {
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int rb = (wm * TM + i) * 32 + 8 * e4 + 4 * hb;
+          const int64_t tr = col0 + cl, tc = row0 + rb;
+          if (tr < g.N && tc < g.M) {
+            float* dst = fin_tall ? fin_out + tr * fin_ld + tc : out + tr * g.N + tc;
+            *reinterpret_cast<float4*>(dst) = make_float4(val[4 * e4], val[4 * e4 + 1], val[4 * e4 + 2], val[4 * e4 + 3]);
+          }
         }
-    } else {
+      }
+      // rotated amaxes of 16-row blocks of every column (the mirrored tile's rows,
+      // or X_{k+1} along m) from registers
+      if (do_cols) {
+        if (g.amax_rotate) {
+          cmax = fmaxf(cmax, rot_cols_max8<0>(val, csg, cs4));
+          cmax = fmaxf(cmax, rot_cols_max8<8>(val, csg, cs4));
+        } else {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) cmax = fmaxf(cmax, fabsf(val[i][j][e]));
+          for (int e = 0; e < 16; ++e) cmax = fmaxf(cmax, fabsf(val[e]));
+        }
+      }
     }
-  }
   __syncthreads();
   // rows of the tile: 32 lanes per row, one 16-byte slot each (coalesced stores;
-  // a quad of lanes holds one 16-column block)
+  // a quad of lanes holds one 16-column block), and the rotated amaxes of
+  // 16-column blocks of every row
   {
     constexpr int kSlots = BN / 4;
     static_assert(NT % kSlots == 0 && (BM * kSlots) % NT == 0, "the row pass covers the tile");
-    const int p = lane & 3;
+    const int pq = lane & 3;
     float sg[4];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) sg[w] = ((g.amax_mask >> (4 * p + w)) & 1u) ? -1.0f : 1.0f;
-    const float s4 = (p & 1) ? -1.0f : 1.0f;
+    for (int w = 0; w < 4; ++w) sg[w] = ((g.amax_mask >> (4 * pq + w)) & 1u) ? -1.0f : 1.0f;
+    const float s4 = (pq & 1) ? -1.0f : 1.0f;
     constexpr int kIt = BM * kSlots / NT;
-    float4 u[kIt];
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
       const int idx = threadIdx.x + NT * it;
-      u[it] = *reinterpret_cast<const float4*>(tile + (idx / kSlots) * kLdT + 4 * (idx % kSlots));
-    }
-#pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      const int idx = threadIdx.x + NT * it;
+      const float4 u = *reinterpret_cast<const float4*>(tile + (idx / kSlots) * kLdT + 4 * (idx % kSlots));
       const int64_t r = row0 + idx / kSlots, c = col0 + 4 * (idx % kSlots);
       if (r < g.M && c < g.N && !fin_tall)
-        *reinterpret_cast<float4*>(fin ? fin_out + r * fin_ld + c : out + r * g.N + c) = u[it];
-    }
-    if (do_rows && g.amax_rotate) {
-#pragma unroll
-      for (int it = 0; it < kIt; ++it) rmax = fmaxf(rmax, rot_rows_max4(u[it], sg, s4));
-    } else if (do_rows) {
-#pragma unroll
-      for (int it = 0; it < kIt; ++it)
-        rmax = fmaxf(rmax, fmaxf(fmaxf(fabsf(u[it].x), fabsf(u[it].y)), fmaxf(fabsf(u[it].z), fabsf(u[it].w))));
+        *reinterpret_cast<float4*>(fin ? fin_out + r * fin_ld + c : out + r * g.N + c) = u;
+      if (do_rows) {
+        if (g.amax_rotate) rmax = fmaxf(rmax, rot_rows_max4(u, sg, s4));
+        else rmax = fmaxf(rmax, fmaxf(fmaxf(fabsf(u.x), fabsf(u.y)), fmaxf(fabsf(u.z), fabsf(u.w))));
+      }
     }
   }
   // one maximum per direction and workgroup, recorded on the workgroup's amax line
@@ -681,7 +597,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
     if (threadIdx.x < 2 && (threadIdx.x == 0 ? do_rows : do_cols)) {
       uint32_t m = 0;
 #pragma unroll
-      for (int w = 0; w < NT / 64; ++w) m = m > red[threadIdx.x][w] ? m : red[threadIdx.x][w];
+      for (int w = 0; w < NW; ++w) m = m > red[threadIdx.x][w] ? m : red[threadIdx.x][w];
       const float mf = g.amax_rotate ? 0.25f * __uint_as_float(m) : __uint_as_float(m);
       amax_record(&g.sc[mat], threadIdx.x == 0 ? g.amax_row_slot : g.amax_col_slot, blockIdx.x, mf);
     }
