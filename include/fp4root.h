@@ -225,7 +225,8 @@ typedef struct {
   uint8_t* m_scales;
   float* m_tensor_scale;
   int64_t rows, cols;
-  float scale;            /* update scale s of this parameter                              */
+  float scale;            /* update scale s of this parameter; 0 selects the default
+                           * fl32(sqrt(max(1, rows / cols))) (Muon's shape factor)         */
 } fp4root_param;
 
 typedef struct {
@@ -243,7 +244,11 @@ size_t fp4root_root_step_workspace(const fp4root_param* params, int64_t count, c
  * seed momentum_seed + p); then one fp4root_orthogonalize of every m in place with
  * `ns` (the p99 clipping, normalisation and NVFP4 NS steps); then
  * fp4root_apply_update of w with m and the parameter's scale.  A NaN or Inf in a
- * gradient reaches m and is reported by fp4root_device_status(ws). */
+ * gradient reaches m and is reported by fp4root_device_status(ws): the status word is
+ * cleared once per call and kept across the stages.  Every argument of every
+ * parameter is checked before the first launch (FP4ROOT_ERR_INVALID_ARG for a null
+ * or misaligned pointer, a negative or non-finite scale, ...), so an error leaves
+ * all states unchanged. */
 int fp4root_root_step(const fp4root_param* params, int64_t count, const fp4root_root_config* rc,
                       const fp4root_ns_config* ns, void* ws, size_t ws_bytes, void* stream);
 

@@ -87,9 +87,10 @@ hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* h
                                  uint32_t* pcnt = nullptr, float eps = 0.0f);
 
 // Frobenius norm of the clipped matrices: sc[i].inv_norm = fl32(1/(||.|| + eps)).
-// partial: chunk.total_tiles doubles of scratch.
+// partial: chunk.total_tiles doubles of scratch.  A NaN or infinite entry sets
+// kStatusNonFinite in *status.
 hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, float eps,
-                           hipStream_t st);
+                           uint32_t* status, hipStream_t st);
 
 // Canonical copy: X_b (m x n, m = min(rows, cols)) = fl32(clamp(M, tau) * inv_norm),
 // transposed when rows > cols.  x: base of the group's canonical buffer, matrix b

@@ -254,7 +254,8 @@ hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* h
 // Frobenius norm of clamp(M, tau): per-block binary64 partials in a fixed
 // order, then one fixed-order sum per matrix (deterministic).
 
-__global__ __launch_bounds__(256) void k_sumsq(MatChunk ch, const MatScalars* sc, double* partial) {
+__global__ __launch_bounds__(256) void k_sumsq(MatChunk ch, const MatScalars* sc, double* partial,
+                                               uint32_t* status) {
   __shared__ double red[256];
   const int64_t tile = blockIdx.x;
   const int mi = find_matrix(ch, tile);
@@ -263,6 +264,7 @@ __global__ __launch_bounds__(256) void k_sumsq(MatChunk ch, const MatScalars* sc
   const int64_t r0 = (tile - d.tile_begin) * kPrepRowsPerBlock;
   const int64_t r1 = r0 + kPrepRowsPerBlock < d.rows ? r0 + kPrepRowsPerBlock : d.rows;
   double acc = 0.0;
+  bool bad = false;   // a NaN or infinite entry (the clamp would hide a NaN)
   for (int64_t r = r0; r < r1; ++r) {
     const float4* row = reinterpret_cast<const float4*>(d.in + r * d.ld_in);
     for (int64_t c = threadIdx.x; c < d.cols / 4; c += 256) {
@@ -270,11 +272,13 @@ __global__ __launch_bounds__(256) void k_sumsq(MatChunk ch, const MatScalars* sc
       const float e[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
+        bad |= !(fabsf(e[j]) <= 3.40282347e38f);
         const double x = (double)fminf(fmaxf(e[j], -tau), tau);
         acc = acc + x * x;
       }
     }
   }
+  if (__builtin_amdgcn_ballot_w64(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(status, kStatusNonFinite);
   red[threadIdx.x] = acc;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
@@ -305,8 +309,8 @@ __global__ __launch_bounds__(256) void k_norm_final(MatChunk ch, MatScalars* sc,
 }
 
 hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, float eps,
-                           hipStream_t st) {
-  hipLaunchKernelGGL(k_sumsq, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, partial);
+                           uint32_t* status, hipStream_t st) {
+  hipLaunchKernelGGL(k_sumsq, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, partial, status);
   hipLaunchKernelGGL(k_norm_final, dim3(ch.count), dim3(256), 0, st, ch, sc, partial, eps);
   return hipGetLastError();
 }
@@ -572,7 +576,8 @@ FP4R_DEV double e2m1_grid(uint32_t idx) {
 // Stochastic rounding of one block's magnitudes (the first-moment state; see
 // fp4root_momentum_update): u holds kf times the rotated block, `scale` is the
 // chosen E4M3 code and `rtn` the round-to-nearest codes with that scale; element
-// i draws SplitMix64 output e0 + i + 1 of `key`.  With x = |u| / r exact
+// e0 + i takes 24 bits of SplitMix64 output (e0 + i) / 2 + 1 of `key` (two elements
+// per output, see below).  With x = |u| / r exact
 // (r = fl32(s s_g)), the floor grid point of x is the nearest one or the one
 // below it (the round-to-nearest quotient is within one ulp of x), and
 // rho (hi - lo) r < (|u| - lo r) 2^24 is exact in binary64 (every term has at

@@ -345,11 +345,6 @@ def fp4root_qadamw_update(w: torch.Tensor, g: torch.Tensor, state: QAdamWState, 
         "fp4root_qadamw_update")
 
 
-def muon_scale(rows: int, cols: int) -> float:
-    """The update scale sqrt(max(1, rows / cols)) (Muon's shape factor)."""
-    return max(1.0, rows / cols) ** 0.5
-
-
 class RootStep:
     """Reusable fp4root_root_step over a fixed list of (BF16 weight, FP32 gradient) pairs.
 
@@ -377,12 +372,14 @@ class RootStep:
             st = MomentumState(1, r, c, device=w.device)
             self.scratch.append(m)
             self.states.append(st)
-            sc = scales[i] if scales is not None else muon_scale(r, c)
+            sc = scales[i] if scales is not None else 0.0   # 0: the library's default scale
             self.params[i] = Param(w.data_ptr(), g.data_ptr(), m.data_ptr(), st.codes.data_ptr(),
                                    st.scales.data_ptr(), st.tensor_scale.data_ptr(), r, c, sc)
         self.count = n
         if coeffs is not None:
             flat = [float(v) for row in coeffs for v in row]
+            if len(flat) != 3 * steps:
+                raise ValueError("coeffs must hold steps rows of (a, b, c)")
             self._coeffs = (ctypes.c_float * len(flat))(*flat)
             cptr = ctypes.cast(self._coeffs, ctypes.POINTER(ctypes.c_float))
         else:

@@ -10,10 +10,9 @@ import pytest
 import torch
 
 from oracle import ns, rht
-from oracle.ns import gram64
 from oracle.quantize import quantize
 from paper_2607_04422_amd import workloads
-from tests.gpu_util import assert_same_nvfp4, gpu_nvfp4, need_gpu, np_, rel_fro, ulp_diff
+from tests.gpu_util import assert_same_nvfp4, gpu_nvfp4, need_gpu, np_, rel_fro
 
 pytestmark = pytest.mark.gpu
 
@@ -43,23 +42,24 @@ def _check_step(x0, a, b, c, flags, seed, step, tr, x1):
     qxt = gpu_nvfp4(tr["qxt_codes"][0], tr["qxt_scales"][0], tr["qxt_sg"])
     assert_same_nvfp4(qx, quantize(x0, 1, signs, ad), "qX")
     assert_same_nvfp4(qxt, quantize(x0, 0, signs, ad), "qXt")
+    # every product is the binary32 rounding of its exact value (the oracle's products
+    # are correctly rounded binary64 sums), so the stages agree bit for bit
     A = np_(tr["A"][0])
-    A_ref = ns.f32((np.float64(qx.sg) ** 2) * gram64(qx.block_values()))
+    A_ref = ns.f32((np.float64(qx.sg) ** 2) * ns.block_dot64(qx))
     assert np.array_equal(A, A.T)
-    assert ulp_diff(A, A_ref).max() <= 1 and np.count_nonzero(A != A_ref) <= max(2, A.size // 10**6)
+    assert np.array_equal(A, A_ref), f"A: {np.count_nonzero(A != A_ref)} of {A.size} differ"
     qa = gpu_nvfp4(tr["qa_codes"][0], tr["qa_scales"][0], tr["qa_sg"])
     assert_same_nvfp4(qa, quantize(A, 1, signs, ad), "qA")
     B = np_(tr["B"][0])
-    P = (np.float64(qa.sg) ** 2) * gram64(qa.block_values())
+    P = (np.float64(qa.sg) ** 2) * ns.block_dot64(qa)
     B_ref = ns.f32(np.float64(np.float32(b)) * A.astype(np.float64) + np.float64(np.float32(c)) * P)
     assert np.array_equal(B, B.T)
-    assert ulp_diff(B, B_ref).max() <= 1 and np.count_nonzero(B != B_ref) <= max(2, B.size // 10**6)
+    assert np.array_equal(B, B_ref), f"B: {np.count_nonzero(B != B_ref)} of {B.size} differ"
     qb = gpu_nvfp4(tr["qb_codes"][0], tr["qb_scales"][0], tr["qb_sg"])
     assert_same_nvfp4(qb, quantize(B, 1, signs, ad), "qB")
-    prod = qb.block_values() @ qxt.block_values().T
     X_ref = ns.f32(np.float64(np.float32(a)) * x0.astype(np.float64)
-                   + np.float64(qb.sg) * np.float64(qxt.sg) * prod)
-    assert ulp_diff(x1, X_ref).max() <= 1 and np.count_nonzero(x1 != X_ref) <= max(2, x1.size // 10**6)
+                   + np.float64(qb.sg) * np.float64(qxt.sg) * ns.block_dot64(qb, qxt))
+    assert np.array_equal(x1, X_ref), f"X: {np.count_nonzero(x1 != X_ref)} of {x1.size} differ"
 
 
 @pytest.mark.parametrize("shape", [(64, 128), (256, 512), (272, 400), (144, 144), (272, 144)])
@@ -85,8 +85,7 @@ def test_ns_step_matches_oracle_step():
     for k, (a, b, c) in enumerate(MIXED):
         ref = ns.ns_step_nvfp4(np_(x), a, b, c, rht.step_signs(5, k), True)
         F.fp4root_ns_step(x, a, b, c, flags=6, seed=5, step=k)
-        assert rel_fro(np_(x), ref) <= TOL
-        assert np.count_nonzero(np_(x) != ref) <= 2
+        assert np.array_equal(np_(x), ref), k
 
 
 def _orth_case(mats, coeffs, flags, seed=0, mode="nvfp4"):
@@ -159,9 +158,17 @@ def test_in_place_and_determinism():
     assert torch.equal(out1, x2)
 
 
-def test_nonfinite_input_reported():
+@pytest.mark.parametrize("flags", ["default", "no_clip", "bf16_no_clip"])
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), -float("inf")])
+def test_nonfinite_input_reported(flags, bad):
+    fl = {"default": F.F_DEFAULT, "no_clip": F.F_HADAMARD | F.F_ADAPTIVE46, "bf16_no_clip": F.F_BF16_PATH}[flags]
     m = workloads.matrix(64, 128, seed=1)
-    m[3, 3] = np.nan
-    orth = F.Orthogonalizer([torch.from_numpy(m).cuda()], steps=1, coeffs=MIXED[:1])
+    m[3, 3] = bad
+    orth = F.Orthogonalizer([torch.from_numpy(m).cuda()], steps=1, coeffs=MIXED[:1], flags=fl)
     orth()
     assert orth.status() == -4
+    # a finite input afterwards clears the report
+    m[3, 3] = 0.5
+    orth2 = F.Orthogonalizer([torch.from_numpy(m).cuda()], steps=1, coeffs=MIXED[:1], flags=fl)
+    orth2()
+    assert orth2.status() == 0

@@ -76,14 +76,41 @@ def test_root_step_two_steps():
             o_ref = ns.orthogonalize(m_t, co, seed=3)
             o_gpu = np_(step.scratch[p])
             assert rel_fro(o_gpu, o_ref) <= 1e-3, (p, t)
-            want = R.apply_update(w_before[p], o_gpu, lr, wd, np.float32(F.muon_scale(r, c)))
+            want = R.apply_update(w_before[p], o_gpu, lr, wd, np.float32(R.muon_scale(r, c)))
             assert np.array_equal(_bf16_bits(ws[p]), want), (p, t)
 
 
-def test_root_step_nonfinite_gradient():
-    w = torch.zeros((32, 64), device="cuda", dtype=torch.bfloat16)
-    g = torch.ones((32, 64), device="cuda")
-    g[1, 2] = float("inf")
-    step = F.RootStep([w], [g], lr=0.01)
+@pytest.mark.parametrize("ns_flags", ["default", "no_clip"])
+@pytest.mark.parametrize("bad", [float("inf"), float("nan")])
+def test_root_step_nonfinite_gradient(ns_flags, bad):
+    # the first of two parameters carries the bad value: neither the second
+    # parameter's first-moment stage nor the orthogonalisation may clear the status
+    flags = F.F_DEFAULT if ns_flags == "default" else F.F_HADAMARD | F.F_ADAPTIVE46
+    ws = [torch.zeros((32, 64), device="cuda", dtype=torch.bfloat16) for _ in range(2)]
+    gs = [torch.ones((32, 64), device="cuda") for _ in range(2)]
+    gs[0][1, 2] = bad
+    step = F.RootStep(ws, gs, lr=0.01, ns_flags=flags)
     step(0)
     assert step.status() == -4
+    gs[0][1, 2] = 1.0
+    step(1)
+    assert step.status() == 0
+
+
+def test_root_step_bad_parameter_leaves_states_unchanged():
+    # a misaligned state pointer in the second parameter fails the call before the
+    # first parameter's state is touched
+    ws = [torch.zeros((32, 64), device="cuda", dtype=torch.bfloat16) for _ in range(2)]
+    gs = [torch.ones((32, 64), device="cuda") for _ in range(2)]
+    step = F.RootStep(ws, gs, lr=0.01)
+    good_codes = step.params[1].m_codes
+    step.params[1].m_codes = good_codes + 1
+    with pytest.raises(F.Fp4RootError):
+        step(0)
+    torch.cuda.synchronize()
+    assert float(step.states[0].tensor_scale[0]) == 0.0
+    assert int(step.states[0].codes.count_nonzero()) == 0
+    assert int(ws[0].view(torch.int16).count_nonzero()) == 0
+    step.params[1].m_codes = good_codes
+    step(0)
+    assert step.status() == 0 and float(step.states[0].tensor_scale[0]) > 0.0

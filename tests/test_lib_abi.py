@@ -106,3 +106,26 @@ def test_binding_refuses_cpu_tensors():
         F.fp4root_quantize(torch.zeros(16, 16))
     with pytest.raises(TypeError):
         F.fp4root_ns_step(torch.zeros(16, 16), 1.0, 0.0, 0.0)
+
+
+def test_root_step_and_qadamw_reject_before_any_launch():
+    # every parameter is checked before the first launch: a bad second parameter
+    # fails the call synchronously (the fake pointers are never dereferenced)
+    lib = _lib()
+    ws = ctypes.c_void_p(0x200000)
+    good = F.Param(0x100000, 0x110000, 0x120000, 0x130000, 0x140000, 0x150000, 64, 128, 0.0)
+    cfg = F.RootConfig(0.01, 0.1, 0.9, 6, 0, 0)
+    ns_cfg = F.NsConfig(5, None, 7, 0.99, 1e-7, 0)
+    for field, value, want in (("m_codes", 0, -1), ("m_codes", 0x130001, -1), ("g", 0x110004, -1),
+                               ("scale", -1.0, -1), ("rows", 72, -2)):
+        bad = F.Param(*[getattr(good, f) for f, _ in F.Param._fields_])
+        setattr(bad, field, value)
+        params = (F.Param * 2)(good, bad)
+        assert lib.fp4root_root_step(params, 2, ctypes.byref(cfg), ctypes.byref(ns_cfg), ws, 1 << 40,
+                                     None) == want, field
+    # quantized-state AdamW: the first-moment output may not overlap the gradient at all
+    n = 4096
+    g = 0x100000
+    for m in (g, g + 64, g - 64):
+        assert lib.fp4root_qadamw_update(0x300000, g, m, n, 0x400000, 0x410000, 0x420000, 0x430000, 0x440000,
+                                         0x450000, 1e-3, 0.1, 0.9, 0.95, 1e-8, 6, 0, 0, ws, 1 << 30, None) == -1
