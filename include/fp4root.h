@@ -140,6 +140,23 @@ int fp4root_quantize(const float* x, int64_t batch, int64_t rows, int64_t cols, 
                      float* tensor_scale, float* clip_threshold, void* ws, size_t ws_bytes,
                      void* stream);
 
+/* fp4root_quantize without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  The same arguments and results as fp4root_quantize; its scratch is
+ * a fixed array in the library (about 0.7 MB per GPU, kept until the process ends)
+ * that covers up to 256 matrices per call.  A larger batch returns
+ * FP4ROOT_ERR_WORKSPACE before any work.
+ *   status: optional device int32 that receives 0, or FP4ROOT_ERR_NONFINITE when a
+ *           NaN or Inf was seen (the workspace query fp4root_device_status has no
+ *           workspace to read here), or NULL.
+ * The scratch of the current device is used, so the stream must belong to it.
+ * Every call on a GPU shares that GPU's scratch: calls that overlap on one GPU
+ * (different streams or threads) race.  No device memory is allocated or freed. */
+int fp4root_quantize_noalloc(const float* x, int64_t batch, int64_t rows, int64_t cols, int64_t ld,
+                             int64_t batch_stride, int axis, uint32_t flags, float clip_quantile,
+                             uint64_t seed, int32_t step, uint8_t* codes, uint8_t* scales,
+                             float* tensor_scale, float* clip_threshold, int32_t* status, void* stream);
+
 /* One NVFP4 Newton-Schulz step (Section 3.4 display equation), in place.
  *   x: device, batch matrices m x n FP32, rows contiguous (row stride n), matrix
  *      stride batch_stride >= m*n; any m, n that are multiples of 16 (m <= n is

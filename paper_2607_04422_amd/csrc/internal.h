@@ -86,6 +86,9 @@ hipError_t launch_clip_threshold(const MatChunk& ch, MatScalars* sc, uint32_t* h
                                  uint32_t* status, hipStream_t st, double* psum = nullptr,
                                  uint32_t* pcnt = nullptr, float eps = 0.0f);
 
+// *out = 0, or -4 (non-finite input seen) from the status word *status.
+hipError_t launch_status_out(const uint32_t* status, int32_t* out, hipStream_t st);
+
 // Frobenius norm of the clipped matrices: sc[i].inv_norm = fl32(1/(||.|| + eps)).
 // partial: chunk.total_tiles doubles of scratch.  A NaN or infinite entry sets
 // kStatusNonFinite in *status.

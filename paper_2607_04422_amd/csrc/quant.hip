@@ -308,6 +308,17 @@ __global__ __launch_bounds__(256) void k_norm_final(MatChunk ch, MatScalars* sc,
   }
 }
 
+// The status code of a call (0, or FP4ROOT_ERR_NONFINITE = -4 when a NaN or Inf
+// was seen) from its device status word, into a caller's device word.
+__global__ void k_status_out(const uint32_t* status, int32_t* out) {
+  if (threadIdx.x == 0) *out = (*status & kStatusNonFinite) ? -4 : 0;
+}
+
+hipError_t launch_status_out(const uint32_t* status, int32_t* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_status_out, dim3(1), dim3(64), 0, st, status, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_inv_norm(const MatChunk& ch, MatScalars* sc, double* partial, float eps,
                            uint32_t* status, hipStream_t st) {
   hipLaunchKernelGGL(k_sumsq, dim3((uint32_t)ch.total_tiles), dim3(256), 0, st, ch, sc, partial, status);

@@ -87,6 +87,9 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.fp4root_quantize.argtypes = [vp, i64, i64, i64, i64, i64, ctypes.c_int, u32, f32, u64, i32,
                                      vp, vp, vp, vp, vp, sz, vp]
     lib.fp4root_quantize.restype = ctypes.c_int
+    lib.fp4root_quantize_noalloc.argtypes = [vp, i64, i64, i64, i64, i64, ctypes.c_int, u32, f32, u64, i32,
+                                             vp, vp, vp, vp, vp, vp]
+    lib.fp4root_quantize_noalloc.restype = ctypes.c_int
     lib.fp4root_ns_step.argtypes = [vp, i64, i64, i64, i64, f32, f32, f32, u32, u64, i32,
                                     ctypes.POINTER(NsTrace), vp, sz, vp]
     lib.fp4root_ns_step.restype = ctypes.c_int
@@ -225,6 +228,27 @@ def fp4root_quantize(x: torch.Tensor, axis: int = 1, flags: int = F_HADAMARD | F
     if x.dim() == 2:
         codes, scales = codes[0], scales[0]
     return codes, scales, sg, tau, ws
+
+
+def fp4root_quantize_noalloc(x: torch.Tensor, out, axis: int = 1, flags: int = F_HADAMARD | F_ADAPTIVE46,
+                             clip_quantile: float = 0.99, seed: int = 0, step: int = 0, stream=None):
+    """fp4root_quantize into caller-owned outputs without a workspace (the library's
+    fixed scratch; at most 256 matrices).  out = (codes, scales, tensor_scale,
+    clip_threshold or None, status or None), shaped as fp4root_quantize returns them
+    (batch first); status is an int32 device tensor of one element."""
+    _need_gpu_f32(x, "x")
+    codes, scales, sg, tau, status = out
+    xb = x if x.dim() == 3 else x.unsqueeze(0)
+    if xb.stride(-1) != 1:
+        raise ValueError("x rows must be contiguous")
+    B, R, C = xb.shape
+    ld = xb.stride(1)
+    bstride = xb.stride(0) if B > 1 else R * ld
+    _check(load().fp4root_quantize_noalloc(_ptr(xb), B, R, C, ld, bstride, axis, flags, clip_quantile, seed, step,
+                                           _ptr(codes), _ptr(scales), _ptr(sg),
+                                           _ptr(tau) if tau is not None else None,
+                                           _ptr(status) if status is not None else None, _stream(stream)),
+           "fp4root_quantize_noalloc")
 
 
 def fp4root_ns_step(x: torch.Tensor, a: float, b: float, c: float,
