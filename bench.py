@@ -30,6 +30,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -111,39 +113,62 @@ def torch_bf16_reference(inputs, coeffs_for, steps, warmup, iters, torch):
     return t
 
 
-def cpu_baseline(case, coeffs_for, steps, sample_matrices=3):
-    """The oracle, as it stands, on a bounded sample of the workload (the first
-    `sample_matrices` 1024 x 3072 matrices of the 3B-shaped set, about 10-20 s on
-    the host), FLOP-scaled to the whole set."""
-    import numpy as np
+def _oracle_sample(m):
+    """The part of a workload matrix the oracle is timed on: the matrix itself when it
+    holds at most 1024 x 3072 elements, else its leading 1024 x 3072 block (3072 x 1024
+    for a tall matrix), drawn from the same distribution."""
+    r, c = m.shape
+    if r * c <= 1024 * 3072:
+        return m
+    if r <= c:
+        return np.ascontiguousarray(m[:min(r, 1024), :min(c, 3072)])
+    return np.ascontiguousarray(m[:min(r, 3072), :min(c, 1024)])
+
+
+def _quantised_elements(m, n, steps):
+    """Elements the NS steps quantise: X along both axes, A and B (m <= n)."""
+    return steps * (2.0 * m * n + 2.0 * m * m)
+
+
+def cpu_baseline(case, coeffs_for, steps):
+    """The oracle, as it stands, on a bounded sample of the workload (one matrix or its
+    leading 1024 x 3072 block, about 10-30 s on the host).  Its time is split into the
+    clip and normalisation (scaled by elements), the quantisations (scaled by quantised
+    elements) and the exact products (scaled by algorithmic FLOP), each scaled to every
+    matrix of the set and summed."""
     from threadpoolctl import threadpool_info
 
     from oracle import ns
     from paper_2607_04422_amd import workloads
 
     shapes = workloads.case_shapes(case)
-    idx = [i for i, (_, r, c) in enumerate(shapes) if min(r, c) == 1024][:sample_matrices]
-    if not idx:
-        idx = [0]
-    mats = workloads.case_matrices(case, limit=max(idx) + 1)
+    first = workloads.case_matrices(case, limit=1)[0]
+    sample = _oracle_sample(first)
+    r0, c0 = sample.shape
+    ms, ns_ = min(r0, c0), max(r0, c0)
+    timing = {}
     t0 = time.perf_counter()
-    f_sample = 0.0
-    for i in idx:
-        m = mats[i]
-        ns.orthogonalize(m, coeffs_for(m.shape[0], m.shape[1]), seed=0)
-        f_sample += ns_flop(min(m.shape), max(m.shape), steps)
+    ns.orthogonalize(sample, coeffs_for(r0, c0), seed=0, timing=timing)
     dt = time.perf_counter() - t0
-    f_set = set_flop([(r, c) for (_, r, c) in shapes], steps)
-    t_set = dt * f_set / f_sample
+    rate_prep = timing.get("prepare", 0.0) / (r0 * c0)
+    rate_q = timing.get("quantize", 0.0) / _quantised_elements(ms, ns_, steps)
+    rate_p = timing.get("products", 0.0) / ns_flop(ms, ns_, steps)
+    t_set = 0.0
+    for (_, r, c) in shapes:
+        m, n = min(r, c), max(r, c)
+        t_set += rate_prep * r * c + rate_q * _quantised_elements(m, n, steps) + rate_p * ns_flop(m, n, steps)
     threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
-    labels = ", ".join(shapes[i][0] for i in idx)
-    r0, c0 = mats[idx[0]].shape
+    label = shapes[0][0]
+    what = "the whole matrix" if sample is first else f"its leading {r0}x{c0} block"
     return {
         "value": len(shapes) / t_set, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
-        "sample": f"{len(idx)} matrices of the set ({labels}; {r0}x{c0}), clip + normalise + {steps} "
-                  f"NVFP4 NS steps each, {dt:.1f} s on the host, scaled by algorithmic FLOP to the "
-                  f"{len(shapes)}-matrix set",
+        "sample": f"{label} ({first.shape[0]}x{first.shape[1]}), {what}: clip + normalise + {steps} NVFP4 NS "
+                  f"steps, {dt:.1f} s on the host ({timing.get('prepare', 0):.1f} s prepare, "
+                  f"{timing.get('quantize', 0):.1f} s quantise, {timing.get('products', 0):.1f} s products); "
+                  f"scaled to the {len(shapes)}-matrix set by elements, quantised elements and algorithmic "
+                  f"FLOP; the products use {threads} BLAS threads, the quantiser one core",
         "sample_seconds": round(dt, 2),
+        "estimated_set_seconds": round(t_set, 1),
         "host_cpu_count": os.cpu_count(),
     }
 
@@ -271,6 +296,7 @@ def main():
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the call")
     ap.add_argument("--no-momentum", action="store_true",
                     help="skip the first-moment state update, the full Root step and Q-AdamW")
     ap.add_argument("--probe", action="store_true",
@@ -321,6 +347,22 @@ def main():
     t_step = time_calls(orth, args.warmup, args.steps, torch, calls)
     value = len(shapes) / t_step
     tflops = flop / t_step / 1e12
+
+    # the same call replayed from a HIP graph (one launch of the recorded kernels)
+    graph_replay = None
+    if not args.no_graph:
+        eager = [o.clone() for o in orth.outputs]
+        graph = orth.capture()
+        graph.replay()
+        torch.cuda.synchronize()
+        same = all(torch.equal(a, b) for a, b in zip(eager, orth.outputs))
+        del eager
+        calls_g = []
+        t_g = time_calls(graph.replay, args.warmup, args.steps, torch, calls_g)
+        graph_replay = {"ms_per_step": round(t_g * 1e3, 4), "per_call_ms": spread(calls_g),
+                        "matrices_per_s": round(len(shapes) / t_g, 2),
+                        "tflops_effective": round(flop / t_g / 1e12, 2), "equals_eager": same}
+        del graph
 
     roofline = None
     if not args.no_roofline:
@@ -384,6 +426,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.case, lambda r, c: F.fp4root_default_coeffs(r, c, S), S)
+        cpu["vs_gpu"] = round(value / cpu["value"], 1)
 
     line = {
         "metric": METRIC, "value": round(value, 3), "unit": "matrices/s", "n_gpus": 1,
@@ -397,6 +440,7 @@ def main():
                    "algorithmic_tflop_per_step": round(flop / 1e12, 3), "parallelism": "single GPU"},
         "tflops_effective": round(tflops, 2),
         "pct_bf16_mfma_peak": round(100 * tflops / BF16_MFMA_PEAK_TFLOPS, 2),
+        "graph_replay": graph_replay,
         "roofline": roofline,
         "bf16_path": bf16,
         "momentum_state_update": momentum,

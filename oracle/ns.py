@@ -26,6 +26,7 @@ Readings taken where the paper is silent:
 from __future__ import annotations
 
 import math
+import time
 
 import numpy as np
 from scipy.linalg.blas import dsyrk
@@ -125,18 +126,35 @@ def normalise(x: np.ndarray, eps: float = 1e-7) -> np.ndarray:
     return (x * inv).astype(np.float32)
 
 
-def ns_step_nvfp4(x, a, b, c, signs=None, adaptive46=True, trace=None):
+class _Clock:
+    """Optional wall-clock accounting of the oracle's parts (for a CPU baseline):
+    seconds spent quantising and in products, added to the dict it is given."""
+
+    def __init__(self, sink):
+        self.sink = sink
+
+    def __call__(self, part, fn, *args):
+        if self.sink is None:
+            return fn(*args)
+        t0 = time.perf_counter()
+        out = fn(*args)
+        self.sink[part] = self.sink.get(part, 0.0) + time.perf_counter() - t0
+        return out
+
+
+def ns_step_nvfp4(x, a, b, c, signs=None, adaptive46=True, trace=None, timing=None):
     """One NVFP4 NS step on a binary32 m x n matrix (Section 3.4 display equation)."""
+    clk = _Clock(timing)
     x = np.asarray(x, dtype=np.float32)
     a64, b64, c64 = (np.float64(np.float32(t)) for t in (a, b, c))
-    qx = quantize(x, 1, signs, adaptive46)
-    qxt = quantize(x, 0, signs, adaptive46)
-    A = f32((np.float64(qx.sg) * np.float64(qx.sg)) * block_dot64(qx))
-    qa = quantize(A, 1, signs, adaptive46)
-    P = (np.float64(qa.sg) * np.float64(qa.sg)) * block_dot64(qa)
+    qx = clk("quantize", quantize, x, 1, signs, adaptive46)
+    qxt = clk("quantize", quantize, x, 0, signs, adaptive46)
+    A = f32((np.float64(qx.sg) * np.float64(qx.sg)) * clk("products", block_dot64, qx))
+    qa = clk("quantize", quantize, A, 1, signs, adaptive46)
+    P = (np.float64(qa.sg) * np.float64(qa.sg)) * clk("products", block_dot64, qa)
     B = f32(b64 * A.astype(np.float64) + c64 * P)
-    qb = quantize(B, 1, signs, adaptive46)
-    prod = block_dot64(qb, qxt)
+    qb = clk("quantize", quantize, B, 1, signs, adaptive46)
+    prod = clk("products", block_dot64, qb, qxt)
     x1 = f32(a64 * x.astype(np.float64) + (np.float64(qb.sg) * np.float64(qxt.sg)) * prod)
     if trace is not None:
         trace.update(qx=qx, qxt=qxt, A=A, qa=qa, B=B, qb=qb)
@@ -208,19 +226,20 @@ def prepare(m, clip_on=True, q=0.99, eps=1e-7):
 
 
 def orthogonalize(m, coeffs, clip_on=True, q=0.99, eps=1e-7, hadamard=True,
-                  adaptive46=True, seed=0, mode="nvfp4"):
+                  adaptive46=True, seed=0, mode="nvfp4", timing=None):
     """Clip, normalise and run len(coeffs) NS steps; returns binary32 in the input's orientation.
 
     mode: "nvfp4" (Section 3.4), "bf16" (plain BF16 comparison path) or "exact"
-    (binary64, no quantisation; returns float64).
+    (binary64, no quantisation; returns float64).  timing: optional dict that
+    receives the seconds spent in "prepare", "quantize" and "products".
     """
-    x, tall, _ = prepare(m, clip_on, q, eps)
+    x, tall, _ = _Clock(timing)("prepare", prepare, m, clip_on, q, eps)
     if mode == "exact":
         x = x.astype(np.float64)
     for k, (a, b, c) in enumerate(coeffs):
         if mode == "nvfp4":
             signs = step_signs(seed, k) if hadamard else None
-            x = ns_step_nvfp4(x, a, b, c, signs, adaptive46)
+            x = ns_step_nvfp4(x, a, b, c, signs, adaptive46, timing=timing)
         elif mode == "bf16":
             x = ns_step_bf16(x, a, b, c)
         elif mode == "exact":

@@ -9,7 +9,9 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfp4root.so")
-SOURCES = ["quant.hip", "gemm_fp4.hip", "gemm_bf16.hip", "optim.hip", "api.cpp"]
+SOURCES = ["quant.hip", "gemm_fp4.hip", "gemm_bf16.hip", "gemm_blaslt.cpp", "optim.hip", "api.cpp"]
+# the update product of the BF16 comparison path is a hipBLASLt GEMM
+LINK_LIBS = ["-L/opt/rocm/lib", "-lhipblaslt", "-Wl,-rpath,/opt/rocm/lib"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -50,7 +52,7 @@ def build(verbose: bool = False, jobs: int = 3, extra_flags=(), out: str = LIB) 
     while procs:
         _wait(procs.pop(0))
     tmp = out + ".tmp"
-    cmd = [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, *LINK_LIBS, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)

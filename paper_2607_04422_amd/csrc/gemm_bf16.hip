@@ -1,9 +1,9 @@
-// BF16 products of the plain Newton-Schulz comparison path on gfx950 MFMA:
-// the same three products as the NVFP4 path (Gram of X, Gram of A with the B
-// epilogue, update of X), on bf16 operands with binary32 accumulation across
-// the whole K loop (MFMA 32x32x16 bf16, accumulators in AGPRs).  Outputs are
-// staged through LDS so that every global store (row-major, mirrored, and the
-// transposed bf16 copy of X) is coalesced.
+// Symmetric BF16 products of the plain Newton-Schulz comparison path on gfx950
+// MFMA: the Gram of X and the Gram of A with the B epilogue, upper tiles only and
+// mirrored, on bf16 operands with binary32 accumulation across the whole K loop
+// (MFMA 32x32x16 bf16, accumulators in AGPRs).  Outputs are staged through LDS so
+// that every global store (row-major and mirrored) is coalesced.  The update
+// product of that path is a library GEMM (gemm_blaslt.cpp).
 #include "device.h"
 #include "internal.h"
 
@@ -99,10 +99,10 @@ __global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int
   __shared__ __attribute__((aligned(16))) char smem[kMain > kEpi ? kMain : kEpi];
   uint16_t(*lds_a)[BM * KS] = reinterpret_cast<uint16_t(*)[BM * KS]>(smem);
   uint16_t(*lds_b)[BN * KS] = reinterpret_cast<uint16_t(*)[BN * KS]>(smem + 2 * BM * KS * sizeof(uint16_t));
-  constexpr bool kSym = MODE != kModeUpdateX;
+  static_assert(MODE == kModeGramA || MODE == kModeGramB, "symmetric products only");
   const int64_t mat = blockIdx.x / tiles_per_mat;
   int tm, tn;
-  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
+  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, true, tm, tn);
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN_, wn = wave % WN_;
@@ -157,7 +157,6 @@ __global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int
   // epilogue: binary32 formula, bf16 rounding, outputs staged in LDS
   uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
   const uint16_t* aux16 = g.aux16 ? g.aux16 + mat * g.out16_bstride : nullptr;
-  float* X = g.x ? g.x + mat * g.x_bstride : nullptr;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -171,10 +170,6 @@ __global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int
         if (r < g.M && c < g.N) {
           float v = acc[i][j][e];
           if (MODE == kModeGramB) v = g.cb * from_bf16(aux16[r * g.N + c]) + g.cc * v;
-          if (MODE == kModeUpdateX) {
-            v = g.ca * X[r * g.N + c] + v;
-            X[r * g.N + c] = v;
-          }
           h = to_bf16(v);
         }
         tile[otile<BN>(rl, cl)] = h;
@@ -189,11 +184,10 @@ __global__ __launch_bounds__(WM_* WN_ * 64) void k_gemm_bf16(GemmBf16Args g, int
     if (r < g.M && c < g.N)
       *reinterpret_cast<uint4*>(o16 + r * g.N + c) = *reinterpret_cast<const uint4*>(tile + otile<BN>(rl, 8 * q));
   }
-  // transposed output: mirrored lower tile (symmetric products) or Xbt (update)
-  const bool transposed = kSym ? (tm != tn) : true;
-  if (transposed) {
-    uint16_t* ot = kSym ? o16 : g.out16t + mat * g.out16t_bstride;
-    const int64_t ldt = kSym ? g.N : g.M;
+  // the mirrored lower tile of an off-diagonal tile
+  if (tm != tn) {
+    uint16_t* ot = o16;
+    const int64_t ldt = g.N;
     constexpr int kRGroups = BM / 8;
     for (int idx = threadIdx.x; idx < BN * kRGroups; idx += NT) {
       const int cl = idx / kRGroups, q = idx % kRGroups;
@@ -219,19 +213,13 @@ hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st
   static_assert(BM == BN, "symmetric products need square tiles");
   static_assert((BM * 8) % NT == 0, "each thread stages whole 16-byte chunks");
   const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
-  const bool sym = mode != kModeUpdateX;
-  const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
+  if (mode == kModeUpdateX || tiles_m != tiles_n) return hipErrorInvalidValue;
+  const int64_t per = (int64_t)tiles_m * (tiles_m + 1) / 2;
   const dim3 grid((uint32_t)(per * g.batch));
-  switch (mode) {
-    case kModeGramA:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    case kModeGramB:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    default:
-      hipLaunchKernelGGL((k_gemm_bf16<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-  }
+  if (mode == kModeGramA)
+    hipLaunchKernelGGL((k_gemm_bf16<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
   return hipGetLastError();
 }
 

@@ -257,22 +257,27 @@ struct GemmBf16Args {
   const uint16_t* b;      // bf16 [N][K] per matrix
   int64_t a_bstride, b_bstride;
   int64_t M, N, K, batch;
-  uint16_t* out16;        // kModeGramA/B: bf16 [M][N] (ld = N); kModeUpdateX: Xb [M][N]
+  uint16_t* out16;        // bf16 [M][N] (ld = N)
   int64_t out16_bstride;
-  uint16_t* out16t;       // kModeUpdateX: Xbt [N][M]
-  int64_t out16t_bstride;
-  float* x;               // kModeUpdateX: FP32 X in place [M][N]
-  int64_t x_bstride;
   const uint16_t* aux16;  // kModeGramB: bf16 A (may equal out16)
-  float ca, cb, cc;
+  float cb, cc;
 };
 
-// Plain BF16 product with FP32 accumulation (the comparison path).
+// Symmetric BF16 products of the comparison path with FP32 accumulation
+// (kModeGramA: X X^T; kModeGramB: b A + c A A^T).
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmBf16Args& g, hipStream_t st);
 
-// Xb = bf16(X), Xbt = bf16(X)^T for a batch of m x n FP32 matrices.
+// Update product of the BF16 path through hipBLASLt: X <- a X + B16 Xb for a batch
+// (B16 [m][m] bf16 with matrix stride m*m, Xb [m][n] bf16 with stride m*n, X [m][n]
+// FP32 with stride x_bstride), FP32 accumulation; ws: ws_bytes of device scratch.
+hipError_t launch_bf16_update_blaslt(const uint16_t* b16, const uint16_t* xb, float* x, int64_t batch, int64_t m,
+                                     int64_t n, int64_t x_bstride, float a, void* ws, size_t ws_bytes,
+                                     hipStream_t st);
+
+// Xb = bf16(X) (round to nearest even) for a batch of m x n FP32 matrices with
+// matrix stride x_bstride; Xb contiguous (stride m*n).
 hipError_t launch_cast_bf16(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
-                            uint16_t* xb, uint16_t* xbt, int64_t b_bstride, hipStream_t st);
+                            uint16_t* xb, hipStream_t st);
 
 // Zero the amax slots selected by `slot_mask` (bit i = slot i) of n scalar
 // records; `full` also resets every tensor scale, tau (+inf) and inv_norm (1).

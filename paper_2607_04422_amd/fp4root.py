@@ -467,6 +467,21 @@ class Orthogonalizer:
                "fp4root_orthogonalize")
         return self.outputs
 
+    def capture(self):
+        """Record one call into a HIP graph (the library allocates nothing and clears
+        its scalars with kernels, so the whole call can be captured); returns the graph,
+        whose replay() repeats the call on the same buffers."""
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self()                       # warm call outside the capture
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(graph, stream=side):
+            self()
+        torch.cuda.synchronize()
+        return graph
+
     def status(self, stream=None) -> int:
         return fp4root_device_status(self.ws, stream)
 

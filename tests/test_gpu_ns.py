@@ -172,3 +172,26 @@ def test_nonfinite_input_reported(flags, bad):
     orth2 = F.Orthogonalizer([torch.from_numpy(m).cuda()], steps=1, coeffs=MIXED[:1], flags=fl)
     orth2()
     assert orth2.status() == 0
+
+
+def test_graph_replay_equals_eager_call():
+    # the whole orthogonalisation recorded in a HIP graph: every replay, with eager
+    # work of the program between the replays, gives the eager call's bits
+    mats = [workloads.matrix(256, 512, seed=3), workloads.matrix(512, 256, seed=4), workloads.matrix(256, 512, seed=5)]
+    ins = [torch.from_numpy(m).cuda() for m in mats]
+    orth = F.Orthogonalizer(ins, steps=5, flags=F.F_DEFAULT, seed=2)
+    eager = [o.clone() for o in orth()]
+    assert orth.status() == 0
+    graph = orth.capture()
+    other = F.Orthogonalizer([torch.from_numpy(workloads.matrix(128, 256, seed=9)).cuda()], steps=2,
+                             coeffs=MIXED[:2], flags=F.F_DEFAULT)
+    for r in range(4):
+        for o in orth.outputs:
+            o.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(eager, orth.outputs)):
+            assert torch.equal(a, b), (r, i)
+        assert orth.status() == 0
+        other()                         # eager work between the replays
+        torch.cuda.synchronize()
