@@ -491,21 +491,12 @@ FP4R_DEV uint32_t dpp_u(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 
-// The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3, and
-// (optionally) the row's e_min over the stage.  All lanes of the wave must be active.
-FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e, uint32_t* emin = nullptr) {
+// The stage bound of the row whose four blocks sit in lanes 4i .. 4i + 3.  All
+// lanes of the wave must be active.
+FP4R_DEV float quad_stage_rho(uint32_t n2, uint32_t e) {
   const uint32_t qn[4] = {dpp_u<0x00>(n2), dpp_u<0x55>(n2), dpp_u<0xAA>(n2), dpp_u<0xFF>(n2)};
   const uint32_t qe[4] = {dpp_u<0x00>(e), dpp_u<0x55>(e), dpp_u<0xAA>(e), dpp_u<0xFF>(e)};
-  if (emin) *emin = min(min(qe[0], qe[1]), min(qe[2], qe[3]));
   return stage_rho(qn, qe);
-}
-
-// rho of a row over two stages from each stage's (rho, e_min): the sums relative
-// to the smaller e_min, formed in binary64 and rounded up (the stage values are
-// already upper bounds).
-FP4R_DEV float pair_rho(float r0, uint32_t e0, float r1, uint32_t e1) {
-  const uint32_t e = min(e0, e1);
-  return ru32(ldexp((double)r0, 2 * (int)(e0 - e)) + ldexp((double)r1, 2 * (int)(e1 - e)));
 }
 
 // Maximum of non-negative values over each 16 lanes / over the wave (compared as

@@ -189,14 +189,13 @@ FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
       v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
       *reinterpret_cast<f16x8*>(lds + lds_kb_base<ROWS>(kb) + lds_row_off(r, half)) = v;
     }
-    // one block at a time: few temporaries while the chain registers of a stage
-    // pair are live
+    // one block at a time: few temporaries live beside the accumulators
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 // Chain records of one operand (see the header): per 64-element stage and 16 rows,
-// [K/64][rows/16], and per stage pair, [K/128][rows/16].  Before the stage loop
+// [K/64][rows/16].  Before the stage loop
 // each wave evaluates rho sigma over its own row groups for every stage (up to
 // kRecStages, K = 32768) into its column of an LDS byte table; the loop reads one
 // byte per stage.

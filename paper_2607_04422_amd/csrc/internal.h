@@ -121,22 +121,7 @@ struct QOut {
   // largest rho over each 16 rows per 64-element stage, [K/64][rows/16]
   float* rhog = nullptr;
   int64_t rhog_bstride = 0;
-  // optional, with rhog: per row and stage {rho of the row (binary32 bits), e_min
-  // of the row}, [K/64][rows], the input of the two-stage records below
-  uint2* rowst = nullptr;
-  int64_t rowst_bstride = 0;
-  // optional, with rhog, single-axis encoder only (K a multiple of 128): the
-  // two-stage records themselves, [K/128][rows/16] (as launch_pair_records
-  // writes them from rowst)
-  float* rho8 = nullptr;
-  int64_t rho8_bstride = 0;
 };
-
-// Two-stage chain records from the per-row stage data: for stage pairs (2p, 2p+1)
-// and 16 rows, the largest rho over the pair's eight blocks, [nstages/2][rows/16]
-// (nstages even).
-hipError_t launch_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_t batch, int64_t rows,
-                               int64_t nstages, float* rho8, int64_t rho8_bstride, hipStream_t st);
 
 // amax over rotated 16-blocks along `axis`; atomically maxes into
 // amax slot `slot` of sc[b].  tau: clamp each element to +-sc[b].tau first when clip != 0.
@@ -220,8 +205,6 @@ struct Fp4Operand {
   int64_t codes_bstride, scales_bstride;
   const float* rhog = nullptr;  // [K/64][rows/16] chain bound records; null: no chaining
   int64_t rhog_bstride = 0;
-  const float* rho8 = nullptr;  // [K/128][rows/16] two-stage records; null: stages chain alone
-  int64_t rho8_bstride = 0;
 };
 
 struct GemmFp4Args {

@@ -639,31 +639,23 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
   }
   // With chain records (axis 1, cols a multiple of 64) each wave takes 16 rows x
   // one 64-column stage: lane 4i + k holds block k of row i, so the stage bound
-  // of a row and the record over the 16 rows reduce within the wave.  With
-  // two-stage records (cols a multiple of 128) waves 2p and 2p + 1 of a group
-  // hold stages 2s and 2s + 1 of the same rows, and exchange their row records.
+  // of a row and the record over the 16 rows reduce within the wave.
   const bool want_rho = AXIS == 1 && out.rhog != nullptr;
-  const bool pairs = want_rho && out.rho8 != nullptr;
-  if (g >= nblk && !pairs) return;   // nblk is a multiple of 64 when records are requested
-  const bool live = g < nblk;        // uniform over a wave when records are requested
+  if (g >= nblk) return;   // nblk is a multiple of 64 when records are requested: whole waves leave
   int64_t r = 0, c = 0;
-  uint32_t rg = 0, st = 0;
   if (want_rho) {
     // the wave index is uniform (waves never straddle a 256-thread group), so the
     // division by the stage count is scalar work
     const uint32_t nst = (uint32_t)(in.cols / 64);
     const uint32_t wv = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 6));
-    rg = wv / nst;
-    st = wv - rg * nst;
+    const uint32_t rg = wv / nst, st = wv - rg * nst;
     const int lane = (int)(threadIdx.x & 63);
     r = (int64_t)rg * 16 + (lane >> 2);
     c = ((int64_t)st * 4 + (lane & 3)) * 16;
   } else {
     block_pos<AXIS>(in, g, r, c);
   }
-  float rrow = 0.0f;
-  uint32_t emin = 15;
-  if (live) {
+  {
     float u[16];
     load_block_at<AXIS>(in, b, r, c, u);
     if (clip) {
@@ -679,10 +671,7 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
     if constexpr (SR)
       codes = sr_block_codes(u, kf, scale, sg, codes, sr_key, (uint64_t)((b * in.rows + r) * in.cols + c));
     if (want_rho) {
-      rrow = quad_stage_rho(n2, block_exp(scale), &emin);
-      if (out.rowst && (threadIdx.x & 3) == 0)
-        out.rowst[b * out.rowst_bstride + (c / 64) * in.rows + r] = make_uint2(__float_as_uint(rrow), emin);
-      const float rho = wave_max_pos(rrow);
+      const float rho = wave_max_pos(quad_stage_rho(n2, block_exp(scale)));
       if ((threadIdx.x & 63) == 0)
         out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
     }
@@ -697,18 +686,6 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
     *reinterpret_cast<uint2*>(out.codes + b * out.codes_bstride + code_off) =
         make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
     out.scales[b * out.scales_bstride + scale_off] = (uint8_t)scale;
-  }
-  if (pairs) {
-    // every wave of the group reaches the barrier (none has returned)
-    __shared__ uint2 odd_rows[2][16];
-    const int w = (int)(threadIdx.x >> 6), i = (int)((threadIdx.x & 63) >> 2);
-    if (live && (w & 1) && (threadIdx.x & 3) == 0) odd_rows[w >> 1][i] = make_uint2(__float_as_uint(rrow), emin);
-    __syncthreads();
-    if (live && !(w & 1)) {
-      const uint2 o = odd_rows[w >> 1][i];
-      const float r8 = wave_max_pos(pair_rho(rrow, emin, __uint_as_float(o.x), o.y));
-      if ((threadIdx.x & 63) == 0) out.rho8[b * out.rho8_bstride + (st / 2) * (in.rows / 16) + rg] = r8;
-    }
   }
 }
 
@@ -773,11 +750,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
     // chain record of this wave's 16 rows for the tile's 64-column stage: lanes
     // 4i .. 4i + 3 hold row i's four blocks (blocks past the edge count as zero)
     if (qx.rhog) {
-      uint32_t emin;
-      const float rrow = quad_stage_rho(n2, e, &emin);
-      if (qx.rowst && (threadIdx.x & 3) == 0 && r < m)
-        qx.rowst[b * qx.rowst_bstride + (c0 / 64) * m + r] = make_uint2(__float_as_uint(rrow), emin);
-      const float rho = wave_max_pos(rrow);
+      const float rho = wave_max_pos(quad_stage_rho(n2, e));
       if ((threadIdx.x & 63) == 0 && r0 + 16 * (threadIdx.x >> 6) < m)
         qx.rhog[b * qx.rhog_bstride + (c0 / 64) * (m / 16) + (r0 / 16) + (threadIdx.x >> 6)] = rho;
     }
@@ -823,35 +796,6 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
   }
 }
 
-// One thread per (stage pair, 16 rows) of a matrix.
-__global__ __launch_bounds__(256) void k_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_t rows,
-                                                      int64_t npairs, float* rho8, int64_t rho8_bstride) {
-  const int64_t b = blockIdx.y;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t groups = rows / 16;
-  if (t >= npairs * groups) return;
-  const int64_t pr = t / groups, gr = t % groups;
-  const uint2* s0 = rowst + b * rowst_bstride + (2 * pr) * rows + 16 * gr;
-  const uint2* s1 = s0 + rows;
-  float m = 0.0f;
-#pragma unroll 4
-  for (int i = 0; i < 16; ++i) {
-    const uint2 a = s0[i], c = s1[i];
-    m = fmaxf(m, pair_rho(__uint_as_float(a.x), a.y, __uint_as_float(c.x), c.y));
-  }
-  rho8[b * rho8_bstride + pr * groups + gr] = m;
-}
-
-hipError_t launch_pair_records(const uint2* rowst, int64_t rowst_bstride, int64_t batch, int64_t rows,
-                               int64_t nstages, float* rho8, int64_t rho8_bstride, hipStream_t st) {
-  const int64_t n = (nstages / 2) * (rows / 16);
-  if (n == 0 || batch == 0) return hipSuccess;
-  const dim3 grid((uint32_t)((n + 255) / 256), (uint32_t)batch);
-  hipLaunchKernelGGL(k_pair_records, grid, dim3(256), 0, st, rowst, rowst_bstride, rows, nstages / 2, rho8,
-                     rho8_bstride);
-  return hipGetLastError();
-}
-
 hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
                             uint32_t sign_mask, bool rotate, bool adaptive46, MatScalars* sc,
                             int slot_n, int slot_m, const QOut& qx, const QOut& qxt, hipStream_t st,
@@ -879,10 +823,8 @@ hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotat
 hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st) {
-  // chain records: row blocks over whole 64-column stages (two-stage records over
-  // whole stage pairs)
+  // chain records: row blocks over whole 64-column stages
   if (out.rhog && (axis != 1 || in.cols % 64 != 0 || in.rows % 16 != 0)) return hipErrorInvalidValue;
-  if (out.rho8 && (!out.rhog || in.cols % 128 != 0)) return hipErrorInvalidValue;
   const int64_t nblk = in.rows * in.cols / 16;
   const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
   if (axis == 1)

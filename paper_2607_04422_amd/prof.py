@@ -6,6 +6,11 @@
         HBM bytes per launch of each kernel from two ``--pmc FETCH_SIZE`` /
         ``--pmc WRITE_SIZE`` runs of ``bench.py --probe``, each counter scaled by
         what it reads for the plain device copy that run ends with
+    python -m paper_2607_04422_amd.prof counters DIR [DIR ...]
+        SQ/GRBM counters of the product kernels from ``--pmc`` runs of
+        ``bench.py --probe`` (each directory one pass), with the derived ratios:
+        matrix-core busy fraction, VALU and binary64 instructions per MFMA, LDS
+        bank-conflict cycles per active LDS cycle, dependency-wait share
 
 The traffic record carries the SHA-256 of the NVFP4 product source, so that a
 reader (bench.py) can tell whether it still describes the kernel in the tree.
@@ -95,9 +100,80 @@ def traffic(fetch_dir: str, write_dir: str, copy_bytes: int):
     return kf, kw, rows
 
 
+# MI355X: 8 XCDs (GRBM_GUI_ACTIVE is summed over them), 256 CUs x 4 SIMDs
+N_XCD = 8
+N_SIMD = 1024
+
+
+def counters(dirs):
+    """{kernel: {counter: mean per dispatch}} over every counter of every directory."""
+    out = collections.OrderedDict()
+    for d in dirs:
+        path = _one(os.path.join(d, "*counter_collection.csv"))
+        acc = collections.OrderedDict()
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                k = short_name(r["Kernel_Name"])
+                acc.setdefault(k, collections.defaultdict(list))[r["Counter_Name"]].append(float(r["Counter_Value"]))
+        for k, cs in acc.items():
+            dst = out.setdefault(k, {})
+            for c, v in cs.items():
+                dst.setdefault(c, sum(v) / len(v))
+    return out
+
+
+def derived(c: dict) -> dict:
+    """Ratios from one kernel's counter means (missing inputs give no entry)."""
+    d = {}
+
+    def have(*names):
+        return all(n in c and c[n] is not None for n in names)
+
+    if have("SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE") and c["GRBM_GUI_ACTIVE"] > 0:
+        d["mfma_busy"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (c["GRBM_GUI_ACTIVE"] / N_XCD * N_SIMD)
+    if have("SQ_INSTS_VALU", "SQ_INSTS_MFMA") and c["SQ_INSTS_MFMA"] > 0:
+        d["valu_per_mfma"] = c["SQ_INSTS_VALU"] / c["SQ_INSTS_MFMA"]
+    if have("SQ_INSTS_VALU_ADD_F64", "SQ_INSTS_MFMA") and c["SQ_INSTS_MFMA"] > 0:
+        d["add_f64_per_mfma"] = c["SQ_INSTS_VALU_ADD_F64"] / c["SQ_INSTS_MFMA"]
+    if have("SQ_INSTS_VALU_CVT", "SQ_INSTS_MFMA") and c["SQ_INSTS_MFMA"] > 0:
+        d["cvt_per_mfma"] = c["SQ_INSTS_VALU_CVT"] / c["SQ_INSTS_MFMA"]
+    if have("SQ_INSTS_LDS", "SQ_INSTS_MFMA") and c["SQ_INSTS_MFMA"] > 0:
+        d["lds_per_mfma"] = c["SQ_INSTS_LDS"] / c["SQ_INSTS_MFMA"]
+    if have("SQ_LDS_BANK_CONFLICT", "SQ_ACTIVE_INST_LDS") and c["SQ_ACTIVE_INST_LDS"] > 0:
+        d["lds_conflict_per_active"] = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_ACTIVE_INST_LDS"]
+    if have("SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES") and c["SQ_WAVE_CYCLES"] > 0:
+        d["wait_share"] = c["SQ_WAIT_INST_ANY"] / c["SQ_WAVE_CYCLES"]
+    if have("SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES") and c["SQ_VALU_MFMA_BUSY_CYCLES"] > 0:
+        d["valu_coexec_share_of_mfma"] = c["SQ_VALU_MFMA_COEXEC_CYCLES"] / c["SQ_VALU_MFMA_BUSY_CYCLES"]
+    return d
+
+
+DERIVED_COLS = ("mfma_busy", "valu_per_mfma", "add_f64_per_mfma", "cvt_per_mfma", "lds_per_mfma",
+                "lds_conflict_per_active", "wait_share", "valu_coexec_share_of_mfma")
+
+
+def _counters_md(dirs) -> str:
+    cs = counters(dirs)
+    keep = [k for k in cs if "k_gemm" in k or "k_encode" in k]
+    lines = ["| kernel | " + " | ".join(DERIVED_COLS) + " |", "|---" * (len(DERIVED_COLS) + 1) + "|"]
+    for k in keep:
+        d = derived(cs[k])
+        lines.append(f"| `{k}` | " + " | ".join(f"{d[c]:.3f}" if c in d else "" for c in DERIVED_COLS) + " |")
+    lines += ["", "Counter means per dispatch:", ""]
+    names = sorted({n for k in keep for n in cs[k]})
+    lines.append("| counter | " + " | ".join(f"`{k}`" for k in keep) + " |")
+    lines.append("|---" * (len(keep) + 1) + "|")
+    for n in names:
+        lines.append(f"| {n} | " + " | ".join(f"{cs[k][n]:.4g}" if n in cs[k] else "" for k in keep) + " |")
+    lines += ["", f"gemm_fp4_source_sha256: {source_sha256()}"]
+    return "\n".join(lines)
+
+
 def _stats_md(directory: str) -> str:
     lines = ["| kernel | calls | total us | average us | % |", "|---|---|---|---|---|"]
     for k, n, tot, avg, pct in stats(directory):
+        if len(k) > 100:   # library kernels (hipBLASLt Cijk_*, torch) named by their first characters
+            k = k[:60] + "..."
         lines.append(f"| `{k}` | {n} | {tot:.1f} | {avg:.1f} | {pct:.2f} |")
     return "\n".join(lines)
 
@@ -133,6 +209,8 @@ def read_update_traffic(path: str):
 def main(argv):
     if len(argv) >= 2 and argv[0] == "stats":
         print(_stats_md(argv[1]))
+    elif len(argv) >= 2 and argv[0] == "counters":
+        print(_counters_md(argv[1:]))
     elif len(argv) >= 3 and argv[0] == "traffic":
         copy_bytes = int(argv[3]) if len(argv) > 3 else 256 << 20
         print(_traffic_md(argv[1], argv[2], copy_bytes))
