@@ -62,13 +62,11 @@ def tile_means(y: np.ndarray) -> np.ndarray:
     return bf16_round((b[:, 0] / TILE).astype(np.float32))
 
 
-def encode_v(v: np.ndarray, signs: np.ndarray | None, adaptive46: bool = True, sqrt: bool = True,
-             mean: bool = True) -> VState:
-    """Second-moment state; ``sqrt`` / ``mean`` switch stages off for the component study
-    (the library always runs the full pipeline)."""
+def encode_v(v: np.ndarray, signs: np.ndarray | None, adaptive46: bool = True) -> VState:
+    """Second-moment state (square root, tile-mean separation, rotation, NVFP4 with BF16 scales)."""
     v = np.asarray(v, np.float32)
-    y = np.sqrt(v).astype(np.float32) if sqrt else v
-    means = tile_means(y) if mean else np.zeros(len(y) // TILE, np.uint16)
+    y = np.sqrt(v).astype(np.float32)
+    means = tile_means(y)
     mu = np.repeat(bf16_value(means), TILE)
     r = (y - mu).astype(np.float32).reshape(-1, 16)
     u = rotate_blocks_f32(r, signs) if signs is not None else r
@@ -98,13 +96,13 @@ def encode_v(v: np.ndarray, signs: np.ndarray | None, adaptive46: bool = True, s
     return VState(codes, best[0].astype(np.uint16), means)
 
 
-def decode_v(st: VState, signs: np.ndarray | None, sqrt: bool = True) -> np.ndarray:
+def decode_v(st: VState, signs: np.ndarray | None) -> np.ndarray:
     q = E2M1_GRID[st.codes & 7]
     q = np.where(st.codes & 8, -q, q).reshape(-1, 16)
     u = (q * bf16_value(st.scales).astype(np.float64)[:, None]).astype(np.float32)   # exact
     r = unrotate_blocks_f32(u, signs) if signs is not None else u
     y = (r.reshape(-1) + np.repeat(bf16_value(st.means), TILE)).astype(np.float32)
-    return (y * y).astype(np.float32) if sqrt else y
+    return (y * y).astype(np.float32)
 
 
 def bias_correction(beta: float, t: int) -> np.float32:

@@ -74,20 +74,24 @@ constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
 
 // LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two
 // 16-byte halves h) of row r at byte
-//   base(kb) + 32 r + 16 (h ^ sw(r)),   base(kb) = 32 ROWS kb + {0, 128, 272, 400}[kb],
-// sw(r) = bit 2 of r xor bit 3 of r.  A 16-byte LDS access is served 16 lanes per
-// cycle over 64 banks (256 bytes).  The MFMA operand reads (16 consecutive rows of
-// one block and half per 16 lanes) then fall in distinct banks through the swizzle,
-// and so do the loader's writes (4 rows x the 4 blocks per 16 lanes) through the
-// block offsets, which are 0, 8, 1 and 9 sixteen-byte units modulo 256 bytes.  The
+//   base(kb) + 32 r + 16 (h ^ sw(r)),   base(kb) = 32 ROWS kb + {0, 16, 64, 80}[kb],
+// sw(r) = bit 2 of r xor bit 3 of r.  gfx950 serves a 16-byte LDS read 16 lanes
+// per cycle over 64 banks (256 bytes) and a 16-byte write 8 lanes per cycle over
+// 32 banks (128 bytes); lanes that share banks in one cycle conflict (measured
+// with the SQ_LDS_BANK_CONFLICT counter on known patterns).  The MFMA operand
+// reads (16 consecutive rows of one block and half per 16 lanes) fall in distinct
+// banks through the swizzle.  The loader's writes (2 rows x the 4 blocks per 8
+// lanes) fall in distinct banks through the block offsets, which are 0, 1, 4 and
+// 5 sixteen-byte units modulo 128 bytes against the rows' 2 units apart.  The
 // offsets are constants, so one address register per operand tile serves every
 // block of both buffers.
 FP4R_DEV int lds_row_off(int row, int h) { return row * 32 + ((h ^ ((row >> 2) & 1) ^ ((row >> 3) & 1)) << 4); }
 template <int ROWS>
-__host__ __device__ constexpr int lds_kb_base(int kb) { return 32 * ROWS * kb + 128 * kb + 16 * (kb >> 1); }
+__host__ __device__ constexpr int lds_kb_base(int kb) { return 32 * ROWS * kb + 16 * ((kb & 1) + 4 * (kb >> 1)); }
 template <int ROWS>
 constexpr int lds_stage_bytes() { return lds_kb_base<ROWS>(3) + 32 * ROWS; }
-static_assert(lds_kb_base<128>(0) == 0 && lds_kb_base<128>(1) % 256 == 128 && lds_kb_base<128>(2) % 256 == 16 && lds_kb_base<128>(3) % 256 == 144,
+static_assert(lds_kb_base<128>(0) % 128 == 0 && lds_kb_base<128>(1) % 128 == 16 && lds_kb_base<128>(2) % 128 == 64 &&
+                  lds_kb_base<128>(3) % 128 == 80,
               "block offsets");
 
 // Output tile coordinates.  Symmetric products enumerate the upper triangle

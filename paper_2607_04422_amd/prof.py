@@ -10,7 +10,11 @@
         SQ/GRBM counters of the product kernels from ``--pmc`` runs of
         ``bench.py --probe`` (each directory one pass), with the derived ratios:
         matrix-core busy fraction, VALU and binary64 instructions per MFMA, LDS
-        bank-conflict cycles per active LDS cycle, dependency-wait share
+        bank-conflict cycles per LDS instruction, dependency-wait share
+    python -m paper_2607_04422_amd.prof lds DIR
+        conflict cycles per LDS instruction of each kernel of a
+        ``--pmc SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT`` run (the calibration
+        program ``probes/lds_banks.hip``)
 
 The traffic record carries the SHA-256 of the NVFP4 product source, so that a
 reader (bench.py) can tell whether it still describes the kernel in the tree.
@@ -40,6 +44,7 @@ def short_name(name: str) -> str:
     name = name.strip().strip('"')
     if name.startswith("void "):
         name = name[5:]
+    name = name.replace("(anonymous namespace)::", "")
     depth = 0
     for i, ch in enumerate(name):
         if ch == "<":
@@ -139,8 +144,8 @@ def derived(c: dict) -> dict:
         d["cvt_per_mfma"] = c["SQ_INSTS_VALU_CVT"] / c["SQ_INSTS_MFMA"]
     if have("SQ_INSTS_LDS", "SQ_INSTS_MFMA") and c["SQ_INSTS_MFMA"] > 0:
         d["lds_per_mfma"] = c["SQ_INSTS_LDS"] / c["SQ_INSTS_MFMA"]
-    if have("SQ_LDS_BANK_CONFLICT", "SQ_ACTIVE_INST_LDS") and c["SQ_ACTIVE_INST_LDS"] > 0:
-        d["lds_conflict_per_active"] = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_ACTIVE_INST_LDS"]
+    if have("SQ_LDS_BANK_CONFLICT", "SQ_INSTS_LDS") and c["SQ_INSTS_LDS"] > 0:
+        d["lds_conflict_per_inst"] = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_INSTS_LDS"]
     if have("SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES") and c["SQ_WAVE_CYCLES"] > 0:
         d["wait_share"] = c["SQ_WAIT_INST_ANY"] / c["SQ_WAVE_CYCLES"]
     if have("SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES") and c["SQ_VALU_MFMA_BUSY_CYCLES"] > 0:
@@ -149,7 +154,7 @@ def derived(c: dict) -> dict:
 
 
 DERIVED_COLS = ("mfma_busy", "valu_per_mfma", "add_f64_per_mfma", "cvt_per_mfma", "lds_per_mfma",
-                "lds_conflict_per_active", "wait_share", "valu_coexec_share_of_mfma")
+                "lds_conflict_per_inst", "wait_share", "valu_coexec_share_of_mfma")
 
 
 def _counters_md(dirs) -> str:
@@ -166,6 +171,16 @@ def _counters_md(dirs) -> str:
     for n in names:
         lines.append(f"| {n} | " + " | ".join(f"{cs[k][n]:.4g}" if n in cs[k] else "" for k in keep) + " |")
     lines += ["", f"gemm_fp4_source_sha256: {source_sha256()}"]
+    return "\n".join(lines)
+
+
+def _lds_md(directory: str) -> str:
+    cs = counters([directory])
+    lines = ["| kernel | SQ_INSTS_LDS | SQ_LDS_BANK_CONFLICT | conflict cycles per LDS instruction |",
+             "|---|---|---|---|"]
+    for k, c in cs.items():
+        n, b = c.get("SQ_INSTS_LDS", 0.0), c.get("SQ_LDS_BANK_CONFLICT", 0.0)
+        lines.append(f"| `{k}` | {n:.6g} | {b:.6g} | {b / n if n else 0.0:.2f} |")
     return "\n".join(lines)
 
 
@@ -211,6 +226,8 @@ def main(argv):
         print(_stats_md(argv[1]))
     elif len(argv) >= 2 and argv[0] == "counters":
         print(_counters_md(argv[1:]))
+    elif len(argv) >= 2 and argv[0] == "lds":
+        print(_lds_md(argv[1]))
     elif len(argv) >= 3 and argv[0] == "traffic":
         copy_bytes = int(argv[3]) if len(argv) > 3 else 256 << 20
         print(_traffic_md(argv[1], argv[2], copy_bytes))
