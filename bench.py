@@ -113,16 +113,19 @@ def torch_bf16_reference(inputs, coeffs_for, steps, warmup, iters, torch):
     return t
 
 
+SAMPLE_SHORT, SAMPLE_LONG = 1024, 3072   # about 5 s of oracle work per sample on a 16-core host
+
+
 def _oracle_sample(m):
     """The part of a workload matrix the oracle is timed on: the matrix itself when it
     holds at most 1024 x 3072 elements, else its leading 1024 x 3072 block (3072 x 1024
     for a tall matrix), drawn from the same distribution."""
     r, c = m.shape
-    if r * c <= 1024 * 3072:
+    if r * c <= SAMPLE_SHORT * SAMPLE_LONG:
         return m
     if r <= c:
-        return np.ascontiguousarray(m[:min(r, 1024), :min(c, 3072)])
-    return np.ascontiguousarray(m[:min(r, 3072), :min(c, 1024)])
+        return np.ascontiguousarray(m[:min(r, SAMPLE_SHORT), :min(c, SAMPLE_LONG)])
+    return np.ascontiguousarray(m[:min(r, SAMPLE_LONG), :min(c, SAMPLE_SHORT)])
 
 
 def _quantised_elements(m, n, steps):
@@ -131,42 +134,56 @@ def _quantised_elements(m, n, steps):
 
 
 def cpu_baseline(case, coeffs_for, steps):
-    """The oracle, as it stands, on a bounded sample of the workload (one matrix or its
-    leading 1024 x 3072 block, about 10-30 s on the host).  Its time is split into the
-    clip and normalisation (scaled by elements), the quantisations (scaled by quantised
-    elements) and the exact products (scaled by algorithmic FLOP), each scaled to every
-    matrix of the set and summed."""
+    """The oracle, as it stands, on a bounded sample of the workload: the first matrix of
+    each distinct shape (at most three shapes), each whole or its leading 1024 x 3072
+    block, about 5 s each on the host.  Its time is split into the clip and
+    normalisation (scaled by elements), the quantisations (scaled by quantised elements)
+    and the exact products (scaled by algorithmic FLOP); the rates over the samples are
+    applied to every matrix of the set and summed."""
     from threadpoolctl import threadpool_info
 
     from oracle import ns
     from paper_2607_04422_amd import workloads
 
     shapes = workloads.case_shapes(case)
-    first = workloads.case_matrices(case, limit=1)[0]
-    sample = _oracle_sample(first)
-    r0, c0 = sample.shape
-    ms, ns_ = min(r0, c0), max(r0, c0)
+    picks, seen = [], set()
+    for i, (_, r, c) in enumerate(shapes):
+        key = (min(r, c), max(r, c))
+        if key not in seen and len(picks) < 3:
+            seen.add(key)
+            picks.append(i)
+    mats = workloads.case_matrices(case, limit=picks[-1] + 1)
     timing = {}
-    t0 = time.perf_counter()
-    ns.orthogonalize(sample, coeffs_for(r0, c0), seed=0, timing=timing)
-    dt = time.perf_counter() - t0
-    rate_prep = timing.get("prepare", 0.0) / (r0 * c0)
-    rate_q = timing.get("quantize", 0.0) / _quantised_elements(ms, ns_, steps)
-    rate_p = timing.get("products", 0.0) / ns_flop(ms, ns_, steps)
+    units = {"prepare": 0.0, "quantize": 0.0, "products": 0.0}
+    parts = []
+    dt = 0.0
+    for i in picks:
+        sample = _oracle_sample(mats[i])
+        r0, c0 = sample.shape
+        ms, ns_ = min(r0, c0), max(r0, c0)
+        t0 = time.perf_counter()
+        ns.orthogonalize(sample, coeffs_for(r0, c0), seed=0, timing=timing)
+        dt += time.perf_counter() - t0
+        units["prepare"] += r0 * c0
+        units["quantize"] += _quantised_elements(ms, ns_, steps)
+        units["products"] += ns_flop(ms, ns_, steps)
+        what = "whole" if sample is mats[i] else f"leading {r0}x{c0} block"
+        parts.append(f"{shapes[i][0]} ({mats[i].shape[0]}x{mats[i].shape[1]}, {what})")
+    del mats
+    rate = {k: timing.get(k, 0.0) / units[k] for k in units}
     t_set = 0.0
     for (_, r, c) in shapes:
         m, n = min(r, c), max(r, c)
-        t_set += rate_prep * r * c + rate_q * _quantised_elements(m, n, steps) + rate_p * ns_flop(m, n, steps)
+        t_set += (rate["prepare"] * r * c + rate["quantize"] * _quantised_elements(m, n, steps)
+                  + rate["products"] * ns_flop(m, n, steps))
     threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
-    label = shapes[0][0]
-    what = "the whole matrix" if sample is first else f"its leading {r0}x{c0} block"
     return {
         "value": len(shapes) / t_set, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
-        "sample": f"{label} ({first.shape[0]}x{first.shape[1]}), {what}: clip + normalise + {steps} NVFP4 NS "
-                  f"steps, {dt:.1f} s on the host ({timing.get('prepare', 0):.1f} s prepare, "
-                  f"{timing.get('quantize', 0):.1f} s quantise, {timing.get('products', 0):.1f} s products); "
-                  f"scaled to the {len(shapes)}-matrix set by elements, quantised elements and algorithmic "
-                  f"FLOP; the products use {threads} BLAS threads, the quantiser one core",
+        "sample": f"{', '.join(parts)}: clip + normalise + {steps} NVFP4 NS steps each, {dt:.1f} s on the host "
+                  f"({timing.get('prepare', 0):.1f} s prepare, {timing.get('quantize', 0):.1f} s quantise, "
+                  f"{timing.get('products', 0):.1f} s products); scaled to the {len(shapes)}-matrix set by "
+                  f"elements, quantised elements and algorithmic FLOP; the products use {threads} BLAS "
+                  f"threads, the quantiser one core",
         "sample_seconds": round(dt, 2),
         "estimated_set_seconds": round(t_set, 1),
         "host_cpu_count": os.cpu_count(),
