@@ -695,9 +695,12 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
 __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
                                                    uint32_t mask, int rotate, int adaptive, MatScalars* sc,
                                                    int slot_n, int slot_m, QOut qx, QOut qxt, uint32_t reset_mask) {
-  // rows padded to 68 floats: 16-byte row slices for the row blocks, and the
-  // 16 lanes of one 128-bit access (4 rows x 4 slices) or 64 consecutive
-  // columns of one row fall in distinct banks
+  // rows padded to 68 floats: 16-byte row slices for the row blocks.  gfx950 serves
+  // a 128-bit LDS read 16 lanes per cycle over 64 banks and a 128-bit write 8 lanes
+  // per cycle over 32 banks: the 16 lanes of one read (4 rows x 4 slices) and 64
+  // consecutive columns of one row fall in distinct banks, and so do the 8 lanes of
+  // one write (2 rows x 4 slices) because lanes with bit 1 of q set store their
+  // four slices in the order k ^ 2
   __shared__ __align__(16) float tile[kT][kT + 4];
   const int64_t b = blockIdx.y;
   const uint32_t tn = (uint32_t)cdiv(n, kT);   // tiles per row of tiles (grid.x < 2^32)
@@ -722,7 +725,10 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       const float4* p = reinterpret_cast<const float4*>(X + (r0 + i) * n + c0 + 16 * q);
       float4* t = reinterpret_cast<float4*>(&tile[i][16 * q]);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) t[k] = p[k];
+      for (int k = 0; k < 4; ++k) {
+        const int kk = k ^ (q & 2);
+        t[kk] = p[kk];
+      }
     }
   }
   __syncthreads();
