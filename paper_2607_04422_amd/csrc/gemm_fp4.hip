@@ -116,7 +116,10 @@ FP4R_DEV void tile_coords(int64_t t, int tiles_m, int tiles_n, bool sym, int& tm
 // NVFP4 operand staging: each thread loads whole 16-element blocks (8 code
 // bytes + 1 scale byte), decodes them to f16 and writes them to LDS.  Block
 // slot idx = thread + NT j (j < kPer) stages row idx / 4, block idx % 4 of the
-// stage: four consecutive lanes read 32 contiguous bytes of codes.
+// stage.  The operands are stage-major (the encoders write them so): the 32 code
+// bytes and 4 scale bytes of one row and stage follow those of the previous row,
+// so a stage of the tile's rows is one contiguous run and lane idx reads bytes
+// 8 idx .. 8 idx + 7 of it (whole 128-byte lines per wave).
 
 template <int ROWS, int NT>
 struct Fp4Stage {
@@ -129,41 +132,49 @@ struct Fp4Stage {
 FP4R_DEV int stage_row(int idx) { return idx >> 2; }
 FP4R_DEV int stage_kb(int idx) { return idx & 3; }
 
-// Raw buffer resources over the tile's rows of codes and scales (the hardware
-// range check returns 0 for rows past the matrix, so the tail tile needs no branch).
 constexpr int kBufWord3 = 0x00020000;          // raw 32-bit data format, no swizzle
 constexpr uint32_t kBufOutOfRange = 0x7FFFFFF0u;
 
+// The tile's rows of one operand: stage 0 of its codes and scales, the bytes from
+// one stage to the next, and how many of its ROWS rows exist (a tail tile has fewer).
 struct Fp4Src {
-  __amdgpu_buffer_rsrc_t codes, scales;
+  const uint8_t* codes;
+  const uint8_t* scales;
+  int64_t code_stage, scale_stage;
+  int live, nstages;
 };
 
 template <int ROWS>
 FP4R_DEV Fp4Src fp4_src(const Fp4Operand& op, int64_t mat, int64_t rows, int64_t K, int64_t row0) {
-  const int64_t nkb = K / 16;
-  const int64_t live = rows - row0 < ROWS ? rows - row0 : ROWS;
   Fp4Src s;
-  s.codes = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(op.codes + mat * op.codes_bstride + row0 * (K / 2)), (short)0, (int)(live * (K / 2)), kBufWord3);
-  s.scales = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(op.scales + mat * op.scales_bstride + row0 * nkb), (short)0, (int)(live * nkb), kBufWord3);
+  s.codes = op.codes + mat * op.codes_bstride + row0 * 32;
+  s.scales = op.scales + mat * op.scales_bstride + row0 * 4;
+  s.code_stage = rows * 32;
+  s.scale_stage = rows * 4;
+  s.live = (int)(rows - row0 < ROWS ? rows - row0 : ROWS);
+  s.nstages = (int)((K + 63) / 64);
   return s;
 }
 
 template <int ROWS, int NT>
 FP4R_DEV void fp4_load(const Fp4Src& src, int nkb, int stage, Fp4Stage<ROWS, NT>& s) {
-  // blocks past the end of K read as 0 (nkb < 2^17)
+  // one buffer resource per stage over the tile's rows of that stage: rows past the
+  // matrix, blocks past the end of K and stages past the last read as 0
+  const bool in_k = stage < src.nstages;
+  const int64_t st = in_k ? stage : 0;
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(src.codes + st * src.code_stage), (short)0, in_k ? src.live * 32 : 0, kBufWord3);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(src.scales + st * src.scale_stage), (short)0, in_k ? src.live * 4 : 0, kBufWord3);
 #pragma unroll
   for (int j = 0; j < Fp4Stage<ROWS, NT>::kPer; ++j) {
     const int idx = (int)threadIdx.x + NT * j;
-    const int kq = stage_kb(idx);
-    const bool valid = stage * 4 + kq < nkb;
-    const uint32_t o = (uint32_t)stage_row(idx) * (uint32_t)nkb + (uint32_t)(kq + 4 * stage);
-    const uint32_t oc = valid ? 8u * o : kBufOutOfRange;
-    const uint32_t os = valid ? o : kBufOutOfRange;
-    const auto c = __builtin_amdgcn_raw_buffer_load_b64(src.codes, (int)oc, 0, 0);
+    const bool valid = stage * 4 + stage_kb(idx) < nkb;
+    const uint32_t oc = valid ? 8u * (uint32_t)idx : kBufOutOfRange;
+    const uint32_t os = valid ? (uint32_t)idx : kBufOutOfRange;
+    const auto c = __builtin_amdgcn_raw_buffer_load_b64(rc, (int)oc, 0, 0);
     s.codes[j] = make_uint2(c[0], c[1]);
-    s.scales[j] = __builtin_amdgcn_raw_buffer_load_b8(src.scales, (int)os, 0, 0);
+    s.scales[j] = __builtin_amdgcn_raw_buffer_load_b8(rs, (int)os, 0, 0);
   }
 }
 

@@ -121,7 +121,22 @@ struct QOut {
   // largest rho over each 16 rows per 64-element stage, [K/64][rows/16]
   float* rhog = nullptr;
   int64_t rhog_bstride = 0;
+  // stage-major layout (the products' operands; axis-1 encoders only): per matrix
+  // codes [ceil(K/64)][rows][32 bytes] and scales [ceil(K/64)][rows][4 bytes], so
+  // that one 64-element stage of consecutive rows is contiguous; otherwise row-major
+  int tiled = 0;
 };
+
+// Bytes of one matrix's codes / scales in the stage-major layout (rows rows, K
+// contraction elements; a last partial stage is padded).
+__host__ __device__ inline int64_t tiled_code_bytes(int64_t rows, int64_t K) { return (K + 63) / 64 * rows * 32; }
+__host__ __device__ inline int64_t tiled_scale_bytes(int64_t rows, int64_t K) { return (K + 63) / 64 * rows * 4; }
+
+// Copy of stage-major codes and scales (batch matrices of rows x K) into the
+// row-major layout (codes rows x K/2, scales rows x K/16 per matrix); a null
+// output is skipped.
+hipError_t launch_untile_nvfp4(const uint8_t* codes, const uint8_t* scales, int64_t batch, int64_t rows,
+                               int64_t K, uint8_t* out_codes, uint8_t* out_scales, hipStream_t st);
 
 // amax over rotated 16-blocks along `axis`; atomically maxes into
 // amax slot `slot` of sc[b].  tau: clamp each element to +-sc[b].tau first when clip != 0.
@@ -200,8 +215,8 @@ hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n,
 enum GemmMode { kModeGramA = 0, kModeGramB = 1, kModeUpdateX = 2 };
 
 struct Fp4Operand {
-  const uint8_t* codes;   // [rows][K/2]
-  const uint8_t* scales;  // [rows][K/16]
+  const uint8_t* codes;   // stage-major: [ceil(K/64)][rows][32 bytes] (QOut::tiled)
+  const uint8_t* scales;  // stage-major: [ceil(K/64)][rows][4 bytes]
   int64_t codes_bstride, scales_bstride;
   const float* rhog = nullptr;  // [K/64][rows/16] chain bound records; null: no chaining
   int64_t rhog_bstride = 0;

@@ -676,7 +676,10 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
         out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
     }
     int64_t code_off, scale_off;
-    if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
+    if (AXIS == 1 && out.tiled) {   // stage-major: [cols/64][rows][32 B], [cols/64][rows][4 B]
+      code_off = ((c / 64) * in.rows + r) * 32 + (c % 64) / 2;
+      scale_off = ((c / 64) * in.rows + r) * 4 + (c % 64) / 16;
+    } else if (AXIS == 1) {   // [rows][cols/2], [rows][cols/16]
       code_off = r * (in.cols / 2) + c / 2;
       scale_off = r * (in.cols / 16) + c / 16;
     } else {           // transposed: [cols][rows/2], [cols][rows/16]
@@ -749,9 +752,10 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       uint64_t codes;
       quant_block(u, sgn, adaptive != 0, scale, codes, n2, qx.rhog != nullptr, kf);
       e = block_exp(scale);
-      *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + r * (n / 2) + c / 2) =
-          make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
-      qx.scales[b * qx.scales_bstride + r * (n / 16) + c / 16] = (uint8_t)scale;
+      const int64_t oc = qx.tiled ? ((c0 / 64) * m + r) * 32 + 8 * q : r * (n / 2) + c / 2;
+      const int64_t os = qx.tiled ? ((c0 / 64) * m + r) * 4 + q : r * (n / 16) + c / 16;
+      *reinterpret_cast<uint2*>(qx.codes + b * qx.codes_bstride + oc) = make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+      qx.scales[b * qx.scales_bstride + os] = (uint8_t)scale;
     }
     // chain record of this wave's 16 rows for the tile's 64-column stage: lanes
     // 4i .. 4i + 3 hold row i's four blocks (blocks past the edge count as zero)
@@ -774,9 +778,10 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       uint64_t codes;
       quant_block(u, sgm, adaptive != 0, scale, codes, n2, qxt.rhog != nullptr, kf);
       e = block_exp(scale);
-      *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + c * (m / 2) + r / 2) =
-          make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
-      qxt.scales[b * qxt.scales_bstride + c * (m / 16) + r / 16] = (uint8_t)scale;
+      const int64_t oc = qxt.tiled ? ((r0 / 64) * n + c) * 32 + 8 * q : c * (m / 2) + r / 2;
+      const int64_t os = qxt.tiled ? ((r0 / 64) * n + c) * 4 + q : c * (m / 16) + r / 16;
+      *reinterpret_cast<uint2*>(qxt.codes + b * qxt.codes_bstride + oc) = make_uint2((uint32_t)codes, (uint32_t)(codes >> 32));
+      qxt.scales[b * qxt.scales_bstride + os] = (uint8_t)scale;
     }
     if (qxt.rhog) {
       // the stage's four blocks of column j sit in the four waves: exchange in LDS
@@ -800,6 +805,36 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
       }
     }
   }
+}
+
+// One thread per (row, stage) of a matrix: 32 code bytes and 4 scale bytes from the
+// stage-major layout to the row-major one (a last partial stage copies its blocks only).
+__global__ __launch_bounds__(256) void k_untile_nvfp4(const uint8_t* codes, const uint8_t* scales, int64_t rows,
+                                                       int64_t K, uint8_t* out_codes, uint8_t* out_scales) {
+  const int64_t b = blockIdx.y;
+  const int64_t nst = (K + 63) / 64;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= rows * nst) return;
+  const int64_t st = t / rows, r = t % rows;
+  const int nb = (int)(K / 16 - 4 * st < 4 ? K / 16 - 4 * st : 4);   // blocks in this stage
+  const uint8_t* sc = codes + b * tiled_code_bytes(rows, K) + (st * rows + r) * 32;
+  const uint8_t* ss = scales + b * tiled_scale_bytes(rows, K) + (st * rows + r) * 4;
+  uint8_t* dc = out_codes ? out_codes + b * rows * (K / 2) + r * (K / 2) + st * 32 : nullptr;
+  uint8_t* ds = out_scales ? out_scales + b * rows * (K / 16) + r * (K / 16) + st * 4 : nullptr;
+  for (int k = 0; k < nb; ++k) {
+    if (out_codes) *reinterpret_cast<uint2*>(dc + 8 * k) = *reinterpret_cast<const uint2*>(sc + 8 * k);
+    if (out_scales) ds[k] = ss[k];
+  }
+}
+
+hipError_t launch_untile_nvfp4(const uint8_t* codes, const uint8_t* scales, int64_t batch, int64_t rows,
+                               int64_t K, uint8_t* out_codes, uint8_t* out_scales, hipStream_t st) {
+  const int64_t n = rows * ((K + 63) / 64);
+  if (n == 0 || batch == 0) return hipSuccess;
+  if (K % 16 != 0) return hipErrorInvalidValue;
+  const dim3 grid((uint32_t)((n + 255) / 256), (uint32_t)batch);
+  hipLaunchKernelGGL(k_untile_nvfp4, grid, dim3(256), 0, st, codes, scales, rows, K, out_codes, out_scales);
+  return hipGetLastError();
 }
 
 hipError_t launch_encode_x2(const float* x, int64_t batch, int64_t m, int64_t n, int64_t x_bstride,
@@ -829,8 +864,9 @@ hipError_t launch_amax(const Batch& in, int axis, uint32_t sign_mask, bool rotat
 hipError_t launch_encode(const Batch& in, int axis, uint32_t sign_mask, bool rotate, bool clip,
                          bool adaptive46, MatScalars* sc, int slot, const QOut& out,
                          float* tensor_scale, hipStream_t st) {
-  // chain records: row blocks over whole 64-column stages
+  // chain records: row blocks over whole 64-column stages; the stage-major layout: row blocks
   if (out.rhog && (axis != 1 || in.cols % 64 != 0 || in.rows % 16 != 0)) return hipErrorInvalidValue;
+  if (out.tiled && axis != 1) return hipErrorInvalidValue;
   const int64_t nblk = in.rows * in.cols / 16;
   const dim3 grid((uint32_t)((nblk + 255) / 256), (uint32_t)in.batch);
   if (axis == 1)
