@@ -45,6 +45,7 @@
 #include "internal.h"
 
 #include <type_traits>
+#include <utility>
 
 namespace fp4r {
 
@@ -316,9 +317,12 @@ enum StageForm { kFormBlock = 0, kFormStage = 1 };
 template <int F>
 using form_t = std::integral_constant<int, F>;
 
+// One output tile of one product: workgroup wg of the product's tiles_per_mat *
+// batch tiles; fin (may be null) routes a last update's output to the callers'
+// matrices.  Every kernel entry below runs this body.
 template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
-void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) {
+FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int tiles_n, int64_t tiles_per_mat,
+                            const GemmFin* finp) {
   constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64, NW = WM_ * WN_;
   // padded row of the FP32 output tile staged in LDS: rows stay 16-byte aligned, and
   // the two half-waves of an MFMA-layout write (rows 4 apart) fall 32 banks apart
@@ -335,9 +339,9 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   char* const lb0 = smem + 2 * kStA;
   char* const lb1 = smem + 2 * kStA + kStB;
   constexpr bool kSym = MODE != kModeUpdateX;
-  const int64_t mat = blockIdx.x / tiles_per_mat;
+  const int64_t mat = wg / tiles_per_mat;
   int tm, tn;
-  tile_coords(blockIdx.x % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
+  tile_coords(wg % tiles_per_mat, tiles_m, tiles_n, kSym, tm, tn);
   const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -521,10 +525,10 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   // transposed tile straight from registers (four consecutive rows of a column
   // form a row segment of it)
   const bool mirror = kSym && tm != tn;
-  const bool fin = !kSym && g.fin_count > 0;
-  float* const fin_out = fin ? g.fin_out[mat] : nullptr;
-  const int64_t fin_ld = fin ? g.fin_ld[mat] : 0;
-  const bool fin_tall = fin && g.fin_tall[mat] != 0;
+  const bool fin = !kSym && finp != nullptr && finp->count > 0;
+  float* const fin_out = fin ? finp->out[mat] : nullptr;
+  const int64_t fin_ld = fin ? finp->ld[mat] : 0;
+  const bool fin_tall = fin && finp->tall[mat] != 0;
   const bool do_rows = g.amax_row_slot >= 0;
   const bool do_cols = g.amax_col_slot >= 0 && (!kSym || mirror);
   float cmax = 0.0f, rmax = 0.0f;
@@ -618,25 +622,81 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat) 
   }
 }
 
-hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st) {
+// One product per launch (its arguments at fixed offsets).
+template <int MODE, int WM_, int WN_, int TM, int TN>
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
+void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat, GemmFin fin) {
+  gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(g, blockIdx.x, tiles_m, tiles_n, tiles_per_mat, &fin);
+}
+
+// Several products of one mode per launch: each workgroup finds its product (uniform
+// over the workgroup) from the cumulative workgroup counts.
+template <int MODE, int WM_, int WN_, int TM, int TN>
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
+void k_gemm_fp4_multi(GemmFp4Batch gb) {
+  int pi = 0;
+  while (pi + 1 < gb.count && (int64_t)blockIdx.x >= gb.wg_end[pi]) ++pi;
+  const int64_t wg = (int64_t)blockIdx.x - (pi > 0 ? gb.wg_end[pi - 1] : 0);
+  gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(gb.p[pi], wg, gb.tiles_m[pi], gb.tiles_n[pi], gb.tiles_per_mat[pi], nullptr);
+}
+
+hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
+                                 const GemmFin* fin) {
   constexpr int WM_ = FP4R_FP4_WAVES_M, WN_ = FP4R_FP4_WAVES_N, TM = FP4R_FP4_TM, TN = FP4R_FP4_TN;
   constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
   static_assert(BM == BN, "symmetric products need square tiles");
   static_assert((BM * 4) % NT == 0, "each thread stages whole blocks");
-  const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
+  if (count < 1 || count > kMaxGemmProblems) return hipErrorInvalidValue;
+  if (fin && fin->count > 0 && (count != 1 || mode != kModeUpdateX || fin->count != list[0].batch))
+    return hipErrorInvalidValue;
+  // longest contraction first: its tiles take the longest, the short ones fill the tail
+  int order[kMaxGemmProblems];
+  for (int i = 0; i < count; ++i) order[i] = i;
+  for (int i = 1; i < count; ++i)
+    for (int j = i; j > 0 && list[order[j]].K > list[order[j - 1]].K; --j) std::swap(order[j], order[j - 1]);
+  GemmFp4Batch gb;
+  gb.count = 0;
+  int64_t total = 0;
   const bool sym = mode != kModeUpdateX;
-  const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
-  const dim3 grid((uint32_t)(per * g.batch));
-  switch (mode) {
-    case kModeGramA:
-      hipLaunchKernelGGL((k_gemm_fp4<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    case kModeGramB:
-      hipLaunchKernelGGL((k_gemm_fp4<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
-      break;
-    default:
-      hipLaunchKernelGGL((k_gemm_fp4<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tiles_m, tiles_n, per);
+  for (int i = 0; i < count; ++i) {
+    const GemmFp4Args& g = list[order[i]];
+    const int tiles_m = (int)((g.M + BM - 1) / BM), tiles_n = (int)((g.N + BN - 1) / BN);
+    const int64_t per = sym ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
+    if (per * g.batch == 0) continue;
+    const int k = gb.count++;
+    gb.p[k] = g;
+    gb.tiles_m[k] = tiles_m;
+    gb.tiles_n[k] = tiles_n;
+    gb.tiles_per_mat[k] = per;
+    total += per * g.batch;
+    gb.wg_end[k] = total;
   }
+  if (gb.count == 0) return hipSuccess;
+  const dim3 grid((uint32_t)total);
+  if (gb.count == 1) {
+    GemmFin f;
+    if (fin) f = *fin;
+    const GemmFp4Args& g = gb.p[0];
+    const int tm = gb.tiles_m[0], tn = gb.tiles_n[0];
+    const int64_t per = gb.tiles_per_mat[0];
+    switch (mode) {
+      case kModeGramA:
+        hipLaunchKernelGGL((k_gemm_fp4<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
+        break;
+      case kModeGramB:
+        hipLaunchKernelGGL((k_gemm_fp4<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
+        break;
+      default:
+        hipLaunchKernelGGL((k_gemm_fp4<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
+    }
+    return hipGetLastError();
+  }
+  // several products per launch: the symmetric products only
+  if ((fin && fin->count > 0) || mode == kModeUpdateX) return hipErrorInvalidValue;
+  if (mode == kModeGramA)
+    hipLaunchKernelGGL((k_gemm_fp4_multi<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, gb);
+  else
+    hipLaunchKernelGGL((k_gemm_fp4_multi<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, gb);
   return hipGetLastError();
 }
 

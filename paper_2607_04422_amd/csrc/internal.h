@@ -237,18 +237,38 @@ struct GemmFp4Args {
   int64_t out_bstride;
   const float* aux;       // kModeGramB: A (may equal out); kModeUpdateX: X_k (may equal out)
   float ca, cb, cc;
-  // kModeUpdateX, last step: when fin_count > 0 the output goes to the callers'
-  // matrices instead of `out`: matrix b to fin_out[b] with row stride fin_ld[b],
-  // transposed (fin_out[b][c][r] = X[r][c]) when fin_tall[b]
-  int fin_count = 0;
-  float* fin_out[kMaxChunk] = {};
-  int64_t fin_ld[kMaxChunk] = {};
-  uint8_t fin_tall[kMaxChunk] = {};
+};
+
+// kModeUpdateX, last step: when count > 0 the output goes to the callers' matrices
+// instead of `out`: matrix b to out[b] with row stride ld[b], transposed
+// (out[b][c][r] = X[r][c]) when tall[b].
+struct GemmFin {
+  int count = 0;
+  float* out[kMaxChunk] = {};
+  int64_t ld[kMaxChunk] = {};
+  uint8_t tall[kMaxChunk] = {};
 };
 
 // NVFP4 product with exact block sums accumulated in binary64.
 // kModeGramA / kModeGramB compute upper-triangle tiles only and mirror them.
-hipError_t launch_gemm_fp4(GemmMode mode, const GemmFp4Args& g, hipStream_t st);
+// Several products of one mode in one launch (up to kMaxGemmProblems): the
+// workgroups of product i follow those of product i - 1, so short products fill
+// the last, partly occupied round of a long one.
+constexpr int kMaxGemmProblems = 4;
+struct GemmFp4Batch {
+  GemmFp4Args p[kMaxGemmProblems];
+  int32_t tiles_m[kMaxGemmProblems], tiles_n[kMaxGemmProblems];
+  int64_t tiles_per_mat[kMaxGemmProblems];
+  int64_t wg_end[kMaxGemmProblems];   // cumulative workgroup counts
+  int32_t count;
+};
+
+// count products of one mode (1 <= count <= kMaxGemmProblems; more than one for the
+// symmetric products only) in one launch, the products with the longest contraction
+// first; fin (host, may be null) routes the output of a single update product to the
+// callers' matrices.
+hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
+                                 const GemmFin* fin = nullptr);
 
 struct GemmBf16Args {
   const uint16_t* a;      // bf16 [M][K] per matrix
