@@ -116,6 +116,16 @@ def test_orthogonalize_mixed_shapes(flags):
     assert max(errs) <= TOL, errs
 
 
+def test_orthogonalize_many_shape_groups():
+    # seven canonical shapes: the symmetric products of one step run in two grouped
+    # launches (four products, then three); contractions that are not multiples of 64,
+    # matrices smaller than one tile, tall inputs; products exact, so outputs equal
+    shapes = [(32, 1024), (272, 400), (208, 80), (144, 144), (48, 48), (112, 336), (64, 64), (400, 272)]
+    mats = [workloads.matrix(r, c, seed=40 + i, kind="normal_outliers") for i, (r, c) in enumerate(shapes)]
+    errs = _orth_case(mats, MIXED, F.F_DEFAULT, seed=12)
+    assert max(errs) == 0.0, errs
+
+
 def test_orthogonalize_bf16_path():
     mats = [workloads.matrix(256, 512, seed=1), workloads.matrix(384, 128, seed=2)]
     errs = _orth_case(mats, MIXED, F.F_CLIP | F.F_BF16_PATH, mode="bf16")
