@@ -211,7 +211,7 @@ FP4R_DEV void fp4_store(char* lds, const Fp4Stage<ROWS, NT>& s) {
 }
 
 // Chain records of one operand (see the header): per 64-element stage and 16 rows,
-// [K/64][rows/16].  Before the stage loop
+// [rows/16][K/64] (group-major).  Before the stage loop
 // each wave evaluates rho sigma over its own row groups for every stage (up to
 // kRecStages, K = 32768) into its column of an LDS byte table; the loop reads one
 // byte per stage.
@@ -371,12 +371,14 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
   const int gb0 = diag ? 0 : wn * TN * 2, ngb = diag ? kGb : TN * 2;
   const float* rec_a = chain_on ? g.a.rhog + mat * g.a.rhog_bstride : nullptr;
   const float* rec_b = chain_on ? g.b.rhog + mat * g.b.rhog_bstride : nullptr;
-  // the largest record over groups g0 .. g0 + ng - 1 of record row `idx`
-  // (missing groups of a tail tile read 0: their rows are zero)
-  auto group_max = [&](const float* rec, int64_t groups_all, int64_t idx, int64_t g0, int ng) {
+  // the largest record of stage `ss` over groups g0 .. g0 + ng - 1 (records are
+  // group-major, [rows/16][K/64], so the lanes of a wave read consecutive stages;
+  // missing groups of a tail tile read 0: their rows are zero)
+  const int64_t nst_all = g.K / 64;
+  auto group_max = [&](const float* rec, int64_t groups_all, int64_t ss, int64_t g0, int ng) {
     float mx = 0.0f;
     for (int k = 0; k < ng; ++k)
-      if (g0 + k < groups_all) mx = fmaxf(mx, rec[idx * groups_all + g0 + k]);
+      if (g0 + k < groups_all) mx = fmaxf(mx, rec[(g0 + k) * nst_all + ss]);
     return mx;
   };
   // chain flags of every stage for this wave's rows into wflags[.][wave] (one

@@ -118,7 +118,7 @@ struct QOut {
   uint8_t* scales;
   int64_t codes_bstride, scales_bstride;
   // optional (axis 1 only, K = cols a multiple of 64): chain bound records, the
-  // largest rho over each 16 rows per 64-element stage, [K/64][rows/16]
+  // largest rho over each 16 rows per 64-element stage, [rows/16][K/64]
   float* rhog = nullptr;
   int64_t rhog_bstride = 0;
   // stage-major layout (the products' operands; axis-1 encoders only): per matrix
@@ -218,7 +218,7 @@ struct Fp4Operand {
   const uint8_t* codes;   // stage-major: [ceil(K/64)][rows][32 bytes] (QOut::tiled)
   const uint8_t* scales;  // stage-major: [ceil(K/64)][rows][4 bytes]
   int64_t codes_bstride, scales_bstride;
-  const float* rhog = nullptr;  // [K/64][rows/16] chain bound records; null: no chaining
+  const float* rhog = nullptr;  // [rows/16][K/64] chain bound records; null: no chaining
   int64_t rhog_bstride = 0;
 };
 

@@ -673,7 +673,7 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
     if (want_rho) {
       const float rho = wave_max_pos(quad_stage_rho(n2, block_exp(scale)));
       if ((threadIdx.x & 63) == 0)
-        out.rhog[b * out.rhog_bstride + (c / 64) * (in.rows / 16) + r / 16] = rho;
+        out.rhog[b * out.rhog_bstride + (r / 16) * (in.cols / 64) + c / 64] = rho;
     }
     int64_t code_off, scale_off;
     if (AXIS == 1 && out.tiled) {   // stage-major: [cols/64][rows][32 B], [cols/64][rows][4 B]
@@ -762,7 +762,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
     if (qx.rhog) {
       const float rho = wave_max_pos(quad_stage_rho(n2, e));
       if ((threadIdx.x & 63) == 0 && r0 + 16 * (threadIdx.x >> 6) < m)
-        qx.rhog[b * qx.rhog_bstride + (c0 / 64) * (m / 16) + (r0 / 16) + (threadIdx.x >> 6)] = rho;
+        qx.rhog[b * qx.rhog_bstride + ((r0 / 16) + (threadIdx.x >> 6)) * (n / 64) + c0 / 64] = rho;
     }
   }
   {
@@ -801,7 +801,7 @@ __global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, in
         }
         const float rho = row16_max_pos(stage_rho(qn, qe));
         if ((j & 15) == 0 && c < n)
-          qxt.rhog[b * qxt.rhog_bstride + (r0 / 64) * (n / 16) + c / 16] = rho;
+          qxt.rhog[b * qxt.rhog_bstride + (c / 16) * (m / 64) + r0 / 64] = rho;
       }
     }
   }
