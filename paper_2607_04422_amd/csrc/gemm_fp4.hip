@@ -34,13 +34,18 @@
 // same binary32 values in the same order and the product stays exactly symmetric)
 // and runs every stage either as one group or as one group per block.
 //
-// Work per wave: a 32 x 64 output tile (1 x 2 MFMA tiles), 32 binary64
-// accumulators and 32 binary32 chain registers per lane; eight waves share a
-// 128 x 128 workgroup tile and two workgroups a CU (four waves per SIMD).  Per
-// MFMA the exact path issues 8 fold instructions (one conversion and one binary64
-// add per output and stage) and 4 decode instructions; per stage a wave waits for
-// its LDS operand reads, for the staged loads of the next stage and at the
-// barrier, which the other waves of its SIMD cover only in part.
+// Work per wave (Gram of qX and update product): a 64 x 64 output tile (2 x 2
+// MFMA tiles), 64 binary64 accumulators and 64 binary32 chain registers per lane;
+// four waves share a 128 x 128 workgroup tile and two workgroups a CU (two waves
+// per SIMD, 236-248 of their 256 VGPRs).  The Gram of qA runs 32 x 64 per wave,
+// eight waves per workgroup, four per SIMD.  Per MFMA the exact path issues 8 fold
+// instructions (one conversion and one binary64 add per output and stage) and 4-5
+// decode instructions; per stage a wave waits for its LDS operand reads, for the
+// staged loads of the next stage and at the barrier, which the other waves of its
+// SIMD cover only in part.  Groups longer than one stage would keep the chain
+// registers live beside the binary64 accumulators, which does not fit: every
+// arrangement tried spilled 36-200 binary32 registers per lane, at 32 x 64 per
+// wave (128 registers) and at 64 x 64 (256).
 #include "device.h"
 #include "internal.h"
 
@@ -53,24 +58,38 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// Tile configuration of the exact NVFP4 product: WAVES_M x WAVES_N waves, each
-// owning TM x TN MFMA 32x32 tiles; K is staged through LDS 64 elements (four
-// NVFP4 blocks) at a time, double-buffered.
-#ifndef FP4R_FP4_WAVES_M
-#define FP4R_FP4_WAVES_M 4
+// Tile configuration of the exact NVFP4 product, per product: WAVES_M x WAVES_N
+// waves, each owning TM x TN MFMA 32x32 tiles, WPE waves per SIMD; K is staged
+// through LDS 64 elements (four NVFP4 blocks) at a time, double-buffered.  Every
+// workgroup tile is 128 x 128.  The Gram of qX and the update product run 64 x 64
+// outputs per wave (four waves per workgroup, two waves per SIMD: half the LDS
+// operand reads per MFMA of a 32 x 64 wave tile); the Gram of qA, with its short
+// contraction, runs 32 x 64 per wave (eight waves, four per SIMD).
+#ifndef FP4R_FP4_CFG_GRAM_X
+#define FP4R_FP4_CFG_GRAM_X 2, 2, 2, 2, 2
 #endif
-#ifndef FP4R_FP4_WAVES_N
-#define FP4R_FP4_WAVES_N 2
+#ifndef FP4R_FP4_CFG_GRAM_A
+#define FP4R_FP4_CFG_GRAM_A 4, 2, 1, 2, 4
 #endif
-#ifndef FP4R_FP4_TM
-#define FP4R_FP4_TM 1
+#ifndef FP4R_FP4_CFG_UPDATE
+#define FP4R_FP4_CFG_UPDATE 2, 2, 2, 2, 2
 #endif
-#ifndef FP4R_FP4_TN
-#define FP4R_FP4_TN 2
+// products (bit = mode) whose operand decode runs at raised wave priority
+#ifndef FP4R_FP4_DECODE_PRIO
+#define FP4R_FP4_DECODE_PRIO 7
 #endif
-#ifndef FP4R_FP4_WAVES_PER_EU
-#define FP4R_FP4_WAVES_PER_EU 4
-#endif
+template <int WM_, int WN_, int TM_, int TN_, int WPE_>
+struct Fp4Tiling {
+  static constexpr int WM = WM_, WN = WN_, TM = TM_, TN = TN_, WPE = WPE_;
+};
+template <int MODE>
+struct Fp4Cfg;
+template <>
+struct Fp4Cfg<kModeGramA> : Fp4Tiling<FP4R_FP4_CFG_GRAM_X> {};
+template <>
+struct Fp4Cfg<kModeGramB> : Fp4Tiling<FP4R_FP4_CFG_GRAM_A> {};
+template <>
+struct Fp4Cfg<kModeUpdateX> : Fp4Tiling<FP4R_FP4_CFG_UPDATE> {};
 constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
 
 // LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two
@@ -404,10 +423,11 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
   // then gets the issue slots ahead of waves still in their MFMA or fold phase, and
   // reaches the barrier sooner (the Gram of qA, with its short K, keeps the default).
   auto put = [&](char* la, char* lb, const Fp4Stage<BM, NT>& xa, const Fp4Stage<BN, NT>& xb) __attribute__((always_inline)) {
-    if constexpr (MODE != kModeGramB) __builtin_amdgcn_s_setprio(1);
+    constexpr bool kPrio = (FP4R_FP4_DECODE_PRIO >> MODE) & 1;
+    if constexpr (kPrio) __builtin_amdgcn_s_setprio(1);
     fp4_store<BM, NT>(la, xa);
     fp4_store<BN, NT>(lb, xb);
-    if constexpr (MODE != kModeGramB) __builtin_amdgcn_s_setprio(0);
+    if constexpr (kPrio) __builtin_amdgcn_s_setprio(0);
   };
 
   const f32x16 zero = {};
@@ -626,7 +646,7 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
 
 // One product per launch (its arguments at fixed offsets).
 template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(Fp4Cfg<MODE>::WPE)))
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat, GemmFin fin) {
   gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(g, blockIdx.x, tiles_m, tiles_n, tiles_per_mat, &fin);
 }
@@ -634,7 +654,7 @@ void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat, 
 // Several products of one mode per launch: each workgroup finds its product (uniform
 // over the workgroup) from the cumulative workgroup counts.
 template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(FP4R_FP4_WAVES_PER_EU)))
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(Fp4Cfg<MODE>::WPE)))
 void k_gemm_fp4_multi(GemmFp4Batch gb) {
   int pi = 0;
   while (pi + 1 < gb.count && (int64_t)blockIdx.x >= gb.wg_end[pi]) ++pi;
@@ -642,12 +662,34 @@ void k_gemm_fp4_multi(GemmFp4Batch gb) {
   gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(gb.p[pi], wg, gb.tiles_m[pi], gb.tiles_n[pi], gb.tiles_per_mat[pi], nullptr);
 }
 
+// Every configuration covers a 128 x 128 output tile with whole blocks per staging thread.
+constexpr int kFp4Tile = 128;
+template <int MODE>
+constexpr bool fp4_cfg_ok() {
+  using C = Fp4Cfg<MODE>;
+  return C::WM * C::TM * 32 == kFp4Tile && C::WN * C::TN * 32 == kFp4Tile &&
+         (kFp4Tile * 4) % (C::WM * C::WN * 64) == 0;
+}
+static_assert(fp4_cfg_ok<kModeGramA>() && fp4_cfg_ok<kModeGramB>() && fp4_cfg_ok<kModeUpdateX>(),
+              "128 x 128 workgroup tiles (square: symmetric products)");
+
+template <int MODE>
+void launch_fp4_single(dim3 grid, hipStream_t st, const GemmFp4Args& g, int tm, int tn, int64_t per,
+                       const GemmFin& f) {
+  using C = Fp4Cfg<MODE>;
+  hipLaunchKernelGGL((k_gemm_fp4<MODE, C::WM, C::WN, C::TM, C::TN>), grid, dim3(C::WM * C::WN * 64), 0, st, g, tm,
+                     tn, per, f);
+}
+template <int MODE>
+void launch_fp4_multi(dim3 grid, hipStream_t st, const GemmFp4Batch& gb) {
+  using C = Fp4Cfg<MODE>;
+  hipLaunchKernelGGL((k_gemm_fp4_multi<MODE, C::WM, C::WN, C::TM, C::TN>), grid, dim3(C::WM * C::WN * 64), 0, st,
+                     gb);
+}
+
 hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
                                  const GemmFin* fin) {
-  constexpr int WM_ = FP4R_FP4_WAVES_M, WN_ = FP4R_FP4_WAVES_N, TM = FP4R_FP4_TM, TN = FP4R_FP4_TN;
-  constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64;
-  static_assert(BM == BN, "symmetric products need square tiles");
-  static_assert((BM * 4) % NT == 0, "each thread stages whole blocks");
+  constexpr int BM = kFp4Tile, BN = kFp4Tile;
   if (count < 1 || count > kMaxGemmProblems) return hipErrorInvalidValue;
   if (fin && fin->count > 0 && (count != 1 || mode != kModeUpdateX || fin->count != list[0].batch))
     return hipErrorInvalidValue;
@@ -682,23 +724,16 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
     const int tm = gb.tiles_m[0], tn = gb.tiles_n[0];
     const int64_t per = gb.tiles_per_mat[0];
     switch (mode) {
-      case kModeGramA:
-        hipLaunchKernelGGL((k_gemm_fp4<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
-        break;
-      case kModeGramB:
-        hipLaunchKernelGGL((k_gemm_fp4<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
-        break;
-      default:
-        hipLaunchKernelGGL((k_gemm_fp4<kModeUpdateX, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, g, tm, tn, per, f);
+      case kModeGramA: launch_fp4_single<kModeGramA>(grid, st, g, tm, tn, per, f); break;
+      case kModeGramB: launch_fp4_single<kModeGramB>(grid, st, g, tm, tn, per, f); break;
+      default: launch_fp4_single<kModeUpdateX>(grid, st, g, tm, tn, per, f);
     }
     return hipGetLastError();
   }
   // several products per launch: the symmetric products only
   if ((fin && fin->count > 0) || mode == kModeUpdateX) return hipErrorInvalidValue;
-  if (mode == kModeGramA)
-    hipLaunchKernelGGL((k_gemm_fp4_multi<kModeGramA, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, gb);
-  else
-    hipLaunchKernelGGL((k_gemm_fp4_multi<kModeGramB, WM_, WN_, TM, TN>), grid, dim3(NT), 0, st, gb);
+  if (mode == kModeGramA) launch_fp4_multi<kModeGramA>(grid, st, gb);
+  else launch_fp4_multi<kModeGramB>(grid, st, gb);
   return hipGetLastError();
 }
 
