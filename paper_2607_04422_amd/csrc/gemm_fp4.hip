@@ -58,21 +58,25 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// Tile configuration of the exact NVFP4 product, per product: WAVES_M x WAVES_N
-// waves, each owning TM x TN MFMA 32x32 tiles, WPE waves per SIMD; K is staged
-// through LDS 64 elements (four NVFP4 blocks) at a time, double-buffered.  Every
-// workgroup tile is 128 x 128.  The Gram of qX and the update product run 64 x 64
-// outputs per wave (four waves per workgroup, two waves per SIMD: half the LDS
-// operand reads per MFMA of a 32 x 64 wave tile); the Gram of qA, with its short
-// contraction, runs 32 x 64 per wave (eight waves, four per SIMD).
-#ifndef FP4R_FP4_CFG_GRAM_X
-#define FP4R_FP4_CFG_GRAM_X 2, 2, 2, 2, 2
+// Tile configurations of the exact NVFP4 product: WAVES_M x WAVES_N waves, each
+// owning TM x TN MFMA 32x32 tiles, WPE waves per SIMD; K is staged through LDS 64
+// elements (four NVFP4 blocks) at a time, double-buffered.  Every workgroup tile is
+// 128 x 128 and two workgroups share a CU.  Wide: 64 x 64 outputs per wave (four
+// waves per workgroup, two per SIMD), half the LDS operand reads per MFMA of
+// Narrow's 32 x 64 per wave (eight waves per workgroup, four per SIMD).  A wide
+// workgroup alone on a CU (the last, partly filled round of a launch) has one wave
+// per SIMD, which cannot overlap MFMA and VALU work, so launches of the Gram of qX
+// and the update product take Wide only when they fill whole rounds of resident
+// workgroups or at least kWideMinRounds of them; the Gram of qA (short
+// contraction) always takes Narrow.
+#ifndef FP4R_FP4_CFG_WIDE
+#define FP4R_FP4_CFG_WIDE 2, 2, 2, 2, 2
 #endif
-#ifndef FP4R_FP4_CFG_GRAM_A
-#define FP4R_FP4_CFG_GRAM_A 4, 2, 1, 2, 4
+#ifndef FP4R_FP4_CFG_NARROW
+#define FP4R_FP4_CFG_NARROW 4, 2, 1, 2, 4
 #endif
-#ifndef FP4R_FP4_CFG_UPDATE
-#define FP4R_FP4_CFG_UPDATE 2, 2, 2, 2, 2
+#ifndef FP4R_FP4_WIDE_MIN_ROUNDS
+#define FP4R_FP4_WIDE_MIN_ROUNDS 4
 #endif
 // products (bit = mode) whose operand decode runs at raised wave priority
 #ifndef FP4R_FP4_DECODE_PRIO
@@ -82,14 +86,9 @@ template <int WM_, int WN_, int TM_, int TN_, int WPE_>
 struct Fp4Tiling {
   static constexpr int WM = WM_, WN = WN_, TM = TM_, TN = TN_, WPE = WPE_;
 };
-template <int MODE>
-struct Fp4Cfg;
-template <>
-struct Fp4Cfg<kModeGramA> : Fp4Tiling<FP4R_FP4_CFG_GRAM_X> {};
-template <>
-struct Fp4Cfg<kModeGramB> : Fp4Tiling<FP4R_FP4_CFG_GRAM_A> {};
-template <>
-struct Fp4Cfg<kModeUpdateX> : Fp4Tiling<FP4R_FP4_CFG_UPDATE> {};
+using Fp4Wide = Fp4Tiling<FP4R_FP4_CFG_WIDE>;
+using Fp4Narrow = Fp4Tiling<FP4R_FP4_CFG_NARROW>;
+constexpr int kWideMinRounds = FP4R_FP4_WIDE_MIN_ROUNDS;
 constexpr int KS = 64;   // K per LDS stage (4 NVFP4 blocks)
 
 // LDS layout of one decoded ROWS x 64 operand stage: block kb (16 f16, two
@@ -645,16 +644,16 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
 }
 
 // One product per launch (its arguments at fixed offsets).
-template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(Fp4Cfg<MODE>::WPE)))
+template <int MODE, int WM_, int WN_, int TM, int TN, int WPE>
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat, GemmFin fin) {
   gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(g, blockIdx.x, tiles_m, tiles_n, tiles_per_mat, &fin);
 }
 
 // Several products of one mode per launch: each workgroup finds its product (uniform
 // over the workgroup) from the cumulative workgroup counts.
-template <int MODE, int WM_, int WN_, int TM, int TN>
-__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(Fp4Cfg<MODE>::WPE)))
+template <int MODE, int WM_, int WN_, int TM, int TN, int WPE>
+__global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void k_gemm_fp4_multi(GemmFp4Batch gb) {
   int pi = 0;
   while (pi + 1 < gb.count && (int64_t)blockIdx.x >= gb.wg_end[pi]) ++pi;
@@ -664,27 +663,25 @@ void k_gemm_fp4_multi(GemmFp4Batch gb) {
 
 // Every configuration covers a 128 x 128 output tile with whole blocks per staging thread.
 constexpr int kFp4Tile = 128;
-template <int MODE>
+template <class C>
 constexpr bool fp4_cfg_ok() {
-  using C = Fp4Cfg<MODE>;
   return C::WM * C::TM * 32 == kFp4Tile && C::WN * C::TN * 32 == kFp4Tile &&
          (kFp4Tile * 4) % (C::WM * C::WN * 64) == 0;
 }
-static_assert(fp4_cfg_ok<kModeGramA>() && fp4_cfg_ok<kModeGramB>() && fp4_cfg_ok<kModeUpdateX>(),
-              "128 x 128 workgroup tiles (square: symmetric products)");
+static_assert(fp4_cfg_ok<Fp4Wide>() && fp4_cfg_ok<Fp4Narrow>(), "128 x 128 workgroup tiles (square: symmetric products)");
+// resident workgroups of a full round: two per CU
+constexpr int64_t kFp4Round = 2 * 256;
 
-template <int MODE>
+template <int MODE, class C>
 void launch_fp4_single(dim3 grid, hipStream_t st, const GemmFp4Args& g, int tm, int tn, int64_t per,
                        const GemmFin& f) {
-  using C = Fp4Cfg<MODE>;
-  hipLaunchKernelGGL((k_gemm_fp4<MODE, C::WM, C::WN, C::TM, C::TN>), grid, dim3(C::WM * C::WN * 64), 0, st, g, tm,
-                     tn, per, f);
+  hipLaunchKernelGGL((k_gemm_fp4<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE>), grid, dim3(C::WM * C::WN * 64), 0, st,
+                     g, tm, tn, per, f);
 }
-template <int MODE>
+template <int MODE, class C>
 void launch_fp4_multi(dim3 grid, hipStream_t st, const GemmFp4Batch& gb) {
-  using C = Fp4Cfg<MODE>;
-  hipLaunchKernelGGL((k_gemm_fp4_multi<MODE, C::WM, C::WN, C::TM, C::TN>), grid, dim3(C::WM * C::WN * 64), 0, st,
-                     gb);
+  hipLaunchKernelGGL((k_gemm_fp4_multi<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE>), grid, dim3(C::WM * C::WN * 64),
+                     0, st, gb);
 }
 
 hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
@@ -717,6 +714,7 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
   }
   if (gb.count == 0) return hipSuccess;
   const dim3 grid((uint32_t)total);
+  const bool wide = total % kFp4Round == 0 || total >= kWideMinRounds * kFp4Round;
   if (gb.count == 1) {
     GemmFin f;
     if (fin) f = *fin;
@@ -724,16 +722,25 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
     const int tm = gb.tiles_m[0], tn = gb.tiles_n[0];
     const int64_t per = gb.tiles_per_mat[0];
     switch (mode) {
-      case kModeGramA: launch_fp4_single<kModeGramA>(grid, st, g, tm, tn, per, f); break;
-      case kModeGramB: launch_fp4_single<kModeGramB>(grid, st, g, tm, tn, per, f); break;
-      default: launch_fp4_single<kModeUpdateX>(grid, st, g, tm, tn, per, f);
+      case kModeGramA:
+        if (wide) launch_fp4_single<kModeGramA, Fp4Wide>(grid, st, g, tm, tn, per, f);
+        else launch_fp4_single<kModeGramA, Fp4Narrow>(grid, st, g, tm, tn, per, f);
+        break;
+      case kModeGramB: launch_fp4_single<kModeGramB, Fp4Narrow>(grid, st, g, tm, tn, per, f); break;
+      default:
+        if (wide) launch_fp4_single<kModeUpdateX, Fp4Wide>(grid, st, g, tm, tn, per, f);
+        else launch_fp4_single<kModeUpdateX, Fp4Narrow>(grid, st, g, tm, tn, per, f);
     }
     return hipGetLastError();
   }
   // several products per launch: the symmetric products only
   if ((fin && fin->count > 0) || mode == kModeUpdateX) return hipErrorInvalidValue;
-  if (mode == kModeGramA) launch_fp4_multi<kModeGramA>(grid, st, gb);
-  else launch_fp4_multi<kModeGramB>(grid, st, gb);
+  if (mode == kModeGramA) {
+    if (wide) launch_fp4_multi<kModeGramA, Fp4Wide>(grid, st, gb);
+    else launch_fp4_multi<kModeGramA, Fp4Narrow>(grid, st, gb);
+  } else {
+    launch_fp4_multi<kModeGramB, Fp4Narrow>(grid, st, gb);
+  }
   return hipGetLastError();
 }
 

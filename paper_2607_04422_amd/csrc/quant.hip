@@ -74,11 +74,30 @@ __global__ __launch_bounds__(256) void k_radix_hist(MatChunk ch, const MatScalar
   uint32_t above = 0;   // elements above prefix p1
   if (threadIdx.x == 0) above_all = 0;
   bool bad = false;
-  for (int64_t r = r0; r < r1; ++r) {
-    const float4* row = reinterpret_cast<const float4*>(d.in + r * d.ld_in);
-    for (int64_t c = threadIdx.x; c < d.cols / 4; c += 256) {
-      const float4 v = row[c];
-      const float e[4] = {v.x, v.y, v.z, v.w};
+  // The block's rows as one sequence of 16-byte quads (row r, quad c), thread t taking
+  // quads t, t + 256, ...; four loads are issued before any is used.
+  const uint32_t c4 = (uint32_t)(d.cols / 4);
+  const uint32_t nq = (uint32_t)(r1 - r0) * c4;
+  uint32_t rr = threadIdx.x / c4, cc = threadIdx.x - rr * c4;   // position of quad threadIdx.x
+  auto step = [&]() {   // advance by 256 quads
+    cc += 256u;
+    while (cc >= c4) {
+      cc -= c4;
+      ++rr;
+    }
+  };
+  for (uint32_t q0 = threadIdx.x; q0 < nq; q0 += 1024u) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      v[u] = q0 + 256u * u < nq ? reinterpret_cast<const float4*>(d.in + (r0 + rr) * d.ld_in)[cc]
+                                : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      step();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (q0 + 256u * u >= nq) break;
+      const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t key = __float_as_uint(e[j]) & 0x7FFFFFFFu;

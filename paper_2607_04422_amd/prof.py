@@ -201,9 +201,13 @@ def _traffic_md(fetch_dir: str, write_dir: str, copy_bytes: int) -> str:
              "|---|---|---|---|---|"]
     for k, n, f, w, b in rows:
         lines.append(f"| `{k}` | {n} | {f:.1f} | {w:.1f} | {b:.4g} |")
+    # the update product's tile configurations together (bench.py's figure is per launch
+    # over every update launch)
     upd = [r for r in rows if r[0].startswith("fp4r::k_gemm_fp4<2")]
     if upd:
-        lines += ["", f"update_product_traffic_bytes_per_launch: {upd[0][4]:.6g}",
+        n = sum(r[1] for r in upd)
+        mean = sum(r[1] * r[4] for r in upd) / n
+        lines += ["", f"update_product_traffic_bytes_per_launch: {mean:.6g}",
                   f"gemm_fp4_source_sha256: {source_sha256()}"]
     return "\n".join(lines)
 
