@@ -328,6 +328,19 @@ const char* fp4root_status_string(int status);
 /* Library version as major*10000 + minor*100 + patch. */
 int fp4root_version(void);
 
+/* ---- product tiling (tests and tuning) --------------------------------------
+ * The NVFP4 products cover each 128 x 128 output tile with four waves of 64 x 64
+ * outputs ("wide") or eight waves of 32 x 64 ("narrow").  By default (mode 0) the
+ * Gram of qX and the update product take the wide form for a launch that fills
+ * whole rounds of resident workgroups (two per CU) or at least four rounds, the
+ * narrow form otherwise; the Gram with the B epilogue always takes the narrow one.
+ * Mode 1 forces the narrow form everywhere, mode 2 the wide form for the Gram of
+ * qX and the update product.  Every product is exact, so outputs are bit for bit
+ * the same in every mode; only the time changes.  The setting is process-wide and
+ * applies to launches issued after the call (calls on other threads race with it).
+ * Returns the previous mode, or FP4ROOT_ERR_INVALID_ARG for a mode outside 0..2. */
+int fp4root_set_product_tiling(int mode);
+
 /* ---- kernel timing for measurement harnesses -------------------------------
  * While enabled, each matrix-product kernel the library launches is bracketed
  * by two HIP events recorded on the stream it is launched on.  Kernel ids:

@@ -49,6 +49,7 @@
 #include "device.h"
 #include "internal.h"
 
+#include <atomic>
 #include <type_traits>
 #include <utility>
 
@@ -684,6 +685,10 @@ void launch_fp4_multi(dim3 grid, hipStream_t st, const GemmFp4Batch& gb) {
                      0, st, gb);
 }
 
+std::atomic<int> g_product_tiling{0};
+
+int swap_product_tiling(int mode) { return g_product_tiling.exchange(mode); }
+
 hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
                                  const GemmFin* fin) {
   constexpr int BM = kFp4Tile, BN = kFp4Tile;
@@ -714,7 +719,8 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
   }
   if (gb.count == 0) return hipSuccess;
   const dim3 grid((uint32_t)total);
-  const bool wide = total % kFp4Round == 0 || total >= kWideMinRounds * kFp4Round;
+  const int forced = g_product_tiling.load(std::memory_order_relaxed);
+  const bool wide = forced == 0 ? (total % kFp4Round == 0 || total >= kWideMinRounds * kFp4Round) : forced == 2;
   if (gb.count == 1) {
     GemmFin f;
     if (fin) f = *fin;

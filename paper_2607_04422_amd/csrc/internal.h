@@ -269,6 +269,9 @@ struct GemmFp4Batch {
 // callers' matrices.
 hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int count, hipStream_t st,
                                  const GemmFin* fin = nullptr);
+// Tile form of the NVFP4 products (0: chosen per launch, 1: narrow, 2: wide; see
+// fp4root_set_product_tiling); returns the previous value.
+int swap_product_tiling(int mode);
 
 struct GemmBf16Args {
   const uint16_t* a;      // bf16 [M][K] per matrix

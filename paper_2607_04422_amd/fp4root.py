@@ -119,6 +119,8 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.fp4root_status_string.restype = ctypes.c_char_p
     lib.fp4root_version.argtypes = []
     lib.fp4root_version.restype = ctypes.c_int
+    lib.fp4root_set_product_tiling.argtypes = [ctypes.c_int]
+    lib.fp4root_set_product_tiling.restype = ctypes.c_int
     lib.fp4root_timer_enable.argtypes = [ctypes.c_int]
     lib.fp4root_timer_enable.restype = ctypes.c_int
     lib.fp4root_timer_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
@@ -167,6 +169,16 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 
 def fp4root_version() -> int:
     return load().fp4root_version()
+
+
+def fp4root_set_product_tiling(mode: int) -> int:
+    """0: tile form chosen per launch, 1: narrow (32 x 64 per wave), 2: wide (64 x 64)
+    for the Gram of qX and the update product; returns the previous mode.  Outputs are
+    the same bits in every mode."""
+    code = load().fp4root_set_product_tiling(int(mode))
+    if code < 0:
+        raise Fp4RootError(code, "fp4root_set_product_tiling")
+    return code
 
 
 def fp4root_timer_enable(on: bool = True):

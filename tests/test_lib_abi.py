@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 def test_host_helpers():
     _lib()
-    assert F.fp4root_version() == 100
+    assert F.fp4root_version() == 200
     assert F.status_string(-3).startswith("workspace")
     co = F.fp4root_default_coeffs(3072, 8192, 5)
     assert len(co) == 5 and all(len(r) == 3 for r in co)
