@@ -714,7 +714,10 @@ __global__ __launch_bounds__(256) void k_encode(Batch in, uint32_t mask, int rot
 // Both quantisations of X from one read: a 64 x 64 tile is staged in LDS; each
 // thread encodes one 16-column block (qX, along n) and one 16-row block (qXt,
 // along m, written transposed).
-__global__ __launch_bounds__(256) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
+// Eight waves per SIMD (64 VGPRs and 24 bytes of scratch per lane) rather than the
+// six its 73 registers would allow: the extra waves cover part of its LDS and
+// memory waits (about 2.5 % less time per launch).
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_encode_x2(const float* x, int64_t m, int64_t n, int64_t x_bstride,
                                                    uint32_t mask, int rotate, int adaptive, MatScalars* sc,
                                                    int slot_n, int slot_m, QOut qx, QOut qxt, uint32_t reset_mask) {
   // rows padded to 68 floats: 16-byte row slices for the row blocks.  gfx950 serves
