@@ -311,6 +311,8 @@ def main():
     ap.add_argument("--case", default="block3b_x4")
     ap.add_argument("--ns-steps", type=int, default=5)
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
+    ap.add_argument("--no-fp32-accum", action="store_true",
+                    help="skip the NVFP4 path with binary32 product accumulation")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the call")
@@ -432,6 +434,41 @@ def main():
         except Exception as exc:   # context only; never fails the bench line
             bf16["torch_bmm_reference"] = {"error": str(exc)[:200]}
 
+    # The same NVFP4 iteration with binary32 product accumulation (FP4ROOT_F_FP32_ACCUM: one
+    # MFMA accumulator per product, as tensor-core NVFP4 products accumulate): its time, its
+    # update product's rate, and its distance to the exact path's output on these inputs.
+    fp32acc = None
+    if not args.no_fp32_accum:
+        orth32 = F.Orthogonalizer(inputs, steps=S, flags=F.F_DEFAULT | F.F_FP32_ACCUM, clip_quantile=0.99,
+                                  eps=1e-7, seed=0)
+        orth32()
+        torch.cuda.synchronize()
+        num = sum(float(torch.sum((a.double() - b.double()) ** 2)) for a, b in zip(orth32.outputs, orth.outputs))
+        den = sum(float(torch.sum(b.double() ** 2)) for b in orth.outputs)
+        calls32 = []
+        t32 = time_calls(orth32, args.warmup, args.steps, torch, calls32)
+        F.fp4root_timer_reset()
+        F.fp4root_timer_enable(True)
+        for _ in range(args.steps):
+            orth32()
+        torch.cuda.synchronize()
+        F.fp4root_timer_enable(False)
+        ms3, n3, fl3 = F.fp4root_timer_read(2)
+        F.fp4root_timer_reset()
+        upd32 = fl3 / (ms3 / 1e3) / 1e12 if ms3 > 0 else 0.0
+        fp32acc = {"ms_per_step": round(t32 * 1e3, 3), "per_call_ms": spread(calls32),
+                   "matrices_per_s": round(len(shapes) / t32, 2),
+                   "tflops_effective": round(flop / t32 / 1e12, 2),
+                   "pct_bf16_mfma_peak": round(100 * flop / t32 / 1e12 / BF16_MFMA_PEAK_TFLOPS, 2),
+                   "update_product_tflops": round(upd32, 2),
+                   "update_product_frac": round(upd32 / F16_MFMA_PEAK_TFLOPS, 4),
+                   "speedup_vs_exact": round(t_step / t32, 3),
+                   "speedup_vs_bf16": round(bf16["ms_per_step"] / (t32 * 1e3), 3) if bf16 else None,
+                   "rel_fro_distance_to_exact": float(np.sqrt(num / den)) if den > 0 else None,
+                   "note": "products accumulate in binary32 in MFMA order (tensor-core style); the "
+                           "quantisers are unchanged; not the oracle-exact path the line's value measures"}
+        del orth32
+
     momentum = None
     root = None
     qadamw = None
@@ -460,6 +497,7 @@ def main():
         "graph_replay": graph_replay,
         "roofline": roofline,
         "bf16_path": bf16,
+        "fp32_accumulation": fp32acc,
         "momentum_state_update": momentum,
         "root_optimizer_step": root,
         "qadamw_step": qadamw,

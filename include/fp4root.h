@@ -70,6 +70,8 @@ enum {
   FP4ROOT_F_ADAPTIVE46 = 4u,  /* adaptive 4/6 block scaling (Section 3.4)                    */
   FP4ROOT_F_BF16_PATH = 8u,   /* plain BF16 Newton-Schulz instead of NVFP4 (comparison path) */
   FP4ROOT_F_STOCHASTIC = 16u, /* stochastic rounding of element codes (momentum state only)  */
+  FP4ROOT_F_FP32_ACCUM = 32u, /* NVFP4 products accumulate in binary32 (MFMA order) instead of
+                                 exactly; see fp4root_orthogonalize                            */
   FP4ROOT_F_DEFAULT = 7u      /* CLIP | HADAMARD | ADAPTIVE46: the paper's route             */
 };
 
@@ -161,8 +163,9 @@ int fp4root_quantize_noalloc(const float* x, int64_t batch, int64_t rows, int64_
  *   x: device, batch matrices m x n FP32, rows contiguous (row stride n), matrix
  *      stride batch_stride >= m*n; any m, n that are multiples of 16 (m <= n is
  *      the efficient orientation: the Gram matrix is m x m);
- *   a, b, c: this step's coefficients; flags: HADAMARD | ADAPTIVE46 | BF16_PATH;
- *   seed, step: select the Hadamard signs; trace: optional export, or NULL. */
+ *   a, b, c: this step's coefficients; flags: HADAMARD | ADAPTIVE46 | BF16_PATH |
+ *   FP32_ACCUM (not with BF16_PATH); seed, step: select the Hadamard signs; trace:
+ *   optional export, or NULL. */
 int fp4root_ns_step(float* x, int64_t batch, int64_t m, int64_t n, int64_t batch_stride,
                     float a, float b, float c, uint32_t flags, uint64_t seed, int32_t step,
                     const fp4root_ns_trace* trace, void* ws, size_t ws_bytes, void* stream);
@@ -170,7 +173,16 @@ int fp4root_ns_step(float* x, int64_t batch, int64_t m, int64_t n, int64_t batch
 /* Batched NVFP4 Root orthogonalisation of `count` matrices (Section 3.4):
  * clip, orient short side first, normalise, cfg->steps NS steps, write back in
  * the input orientation.  Matrices of equal (short, long) shape are batched
- * into the same kernel launches. */
+ * into the same kernel launches.
+ * Products: by default every product of the iteration is the binary32 rounding of
+ * its exact value (exact block products chained where provably exact, binary64
+ * accumulation), so the result equals the binary64-accumulating reference.  With
+ * FP4ROOT_F_FP32_ACCUM (not with FP4ROOT_F_BF16_PATH) each product instead
+ * accumulates its exact 16-element block products in one binary32 MFMA accumulator
+ * over the whole contraction, as tensor-core NVFP4 products accumulate in FP32: the
+ * quantisers are unchanged, each product is within the binary32 accumulation bound
+ * of its exact value, and the rounding differences then grow through the
+ * re-quantisations of later steps, so the output no longer equals the reference. */
 int fp4root_orthogonalize(const fp4root_matrix* mats, int64_t count,
                           const fp4root_ns_config* cfg, void* ws, size_t ws_bytes,
                           void* stream);

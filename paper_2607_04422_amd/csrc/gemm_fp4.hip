@@ -332,14 +332,14 @@ FP4R_DEV uint32_t wave_max_bits(float v) {
 
 // Accumulation form of one stage (uniform over a wave): one group per block, or
 // the stage as one group.
-enum StageForm { kFormBlock = 0, kFormStage = 1 };
+enum StageForm { kFormBlock = 0, kFormStage = 1, kFormRun = 2 };
 template <int F>
 using form_t = std::integral_constant<int, F>;
 
 // One output tile of one product: workgroup wg of the product's tiles_per_mat *
 // batch tiles; fin (may be null) routes a last update's output to the callers'
 // matrices.  Every kernel entry below runs this body.
-template <int MODE, int WM_, int WN_, int TM, int TN>
+template <int MODE, int WM_, int WN_, int TM, int TN, bool ACC32>
 FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int tiles_n, int64_t tiles_per_mat,
                             const GemmFin* finp) {
   constexpr int BM = WM_ * TM * 32, BN = WN_ * TN * 32, NT = WM_ * WN_ * 64, NW = WM_ * WN_;
@@ -416,7 +416,7 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
       if (ss < kRecStages) wflags[ss][wave] = (uint8_t)f;
     }
   };
-  auto stage_flags = [&](int s) { return s < kRecStages ? (uint32_t)wflags[s][wave] : 0u; };
+  auto stage_flags = [&](int s) { return !ACC32 && s < kRecStages ? (uint32_t)wflags[s][wave] : 0u; };
 
   // stage -> LDS buffers (decoded operands)
   // The decode runs at raised wave priority: a wave that has finished its MFMAs
@@ -439,7 +439,9 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
   // MFMAs of the stage in (la, lb).  A group starts with accumulator input 0 and
   // is folded into binary64 as soon as it ends (after its last block, or at the end
   // of the stage), so the chain registers are dead while the next stage decodes.
-  // Blocks past the end of K are zero in LDS and join any group.
+  // Form Run (binary32 accumulation) adds every block to the chain registers, which
+  // start at zero before the first stage and are never folded.  Blocks past the end
+  // of K are zero in LDS and join any group.
   auto compute = [&](auto form_tag, const char* la, const char* lb) __attribute__((always_inline)) {
     constexpr int F = decltype(form_tag)::value;
 #pragma unroll
@@ -457,7 +459,7 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const bool fresh = F == kFormBlock || kb == 0;
+          const bool fresh = F == kFormBlock || (F == kFormStage && kb == 0);
           p[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], fresh ? zero : p[i][j], 0, 0, 0);
         }
       __builtin_amdgcn_sched_barrier(0);   // keep operand loads next to their use
@@ -470,16 +472,29 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    if constexpr (F != kFormRun) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fold(i, j);
+    }
+  };
+  // one stage that is a group of its own (form Stage) or folds every block (Block);
+  // with binary32 accumulation every stage continues the one chain (form Run)
+  auto run_single = [&](uint32_t f, const char* la, const char* lb) __attribute__((always_inline)) {
+    if constexpr (ACC32) {
+      compute(form_t<kFormRun>(), la, lb);
+    } else {
+      if (f & 1u) compute(form_t<kFormStage>(), la, lb);
+      else compute(form_t<kFormBlock>(), la, lb);
+    }
+  };
+  if constexpr (ACC32) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fold(i, j);
-  };
-  // one stage that is a group of its own (form Stage) or folds every block (Block)
-  auto run_single = [&](uint32_t f, const char* la, const char* lb) __attribute__((always_inline)) {
-    if (f & 1u) compute(form_t<kFormStage>(), la, lb);
-    else compute(form_t<kFormBlock>(), la, lb);
-  };
+      for (int j = 0; j < TN; ++j) p[i][j] = zero;
+  }
 
   Fp4Stage<BM, NT> sa;
   Fp4Stage<BN, NT> sb;
@@ -489,7 +504,7 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
   // stage 1 loads while the flags are computed (reads 0 past the last stage)
   fp4_load<BM, NT>(src_a, nkb, 1, sa);
   fp4_load<BN, NT>(src_b, nkb, 1, sb);
-  fill_flags();
+  if constexpr (!ACC32) fill_flags();
   __syncthreads();
   // Two stages per iteration with the LDS buffers as constants: stage s computes
   // from one buffer while stage s + 1, loaded during the previous stage, decodes
@@ -513,6 +528,14 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
       fp4_load<BN, NT>(src_b, nkb, s + 3, sb);
     }
     __syncthreads();
+  }
+  if constexpr (ACC32) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = (double)p[i][j][e];
   }
 
   // epilogue: binary64 formula, one rounding to binary32, staged through LDS
@@ -645,21 +668,22 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
 }
 
 // One product per launch (its arguments at fixed offsets).
-template <int MODE, int WM_, int WN_, int TM, int TN, int WPE>
+template <int MODE, int WM_, int WN_, int TM, int TN, int WPE, bool ACC32>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void k_gemm_fp4(GemmFp4Args g, int tiles_m, int tiles_n, int64_t tiles_per_mat, GemmFin fin) {
-  gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(g, blockIdx.x, tiles_m, tiles_n, tiles_per_mat, &fin);
+  gemm_fp4_tile<MODE, WM_, WN_, TM, TN, ACC32>(g, blockIdx.x, tiles_m, tiles_n, tiles_per_mat, &fin);
 }
 
 // Several products of one mode per launch: each workgroup finds its product (uniform
 // over the workgroup) from the cumulative workgroup counts.
-template <int MODE, int WM_, int WN_, int TM, int TN, int WPE>
+template <int MODE, int WM_, int WN_, int TM, int TN, int WPE, bool ACC32>
 __global__ __launch_bounds__(WM_* WN_ * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void k_gemm_fp4_multi(GemmFp4Batch gb) {
   int pi = 0;
   while (pi + 1 < gb.count && (int64_t)blockIdx.x >= gb.wg_end[pi]) ++pi;
   const int64_t wg = (int64_t)blockIdx.x - (pi > 0 ? gb.wg_end[pi - 1] : 0);
-  gemm_fp4_tile<MODE, WM_, WN_, TM, TN>(gb.p[pi], wg, gb.tiles_m[pi], gb.tiles_n[pi], gb.tiles_per_mat[pi], nullptr);
+  gemm_fp4_tile<MODE, WM_, WN_, TM, TN, ACC32>(gb.p[pi], wg, gb.tiles_m[pi], gb.tiles_n[pi], gb.tiles_per_mat[pi],
+                                              nullptr);
 }
 
 // Every configuration covers a 128 x 128 output tile with whole blocks per staging thread.
@@ -673,16 +697,44 @@ static_assert(fp4_cfg_ok<Fp4Wide>() && fp4_cfg_ok<Fp4Narrow>(), "128 x 128 workg
 // resident workgroups of a full round: two per CU
 constexpr int64_t kFp4Round = 2 * 256;
 
-template <int MODE, class C>
+template <int MODE, class C, bool ACC32>
 void launch_fp4_single(dim3 grid, hipStream_t st, const GemmFp4Args& g, int tm, int tn, int64_t per,
                        const GemmFin& f) {
-  hipLaunchKernelGGL((k_gemm_fp4<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE>), grid, dim3(C::WM * C::WN * 64), 0, st,
-                     g, tm, tn, per, f);
+  hipLaunchKernelGGL((k_gemm_fp4<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE, ACC32>), grid, dim3(C::WM * C::WN * 64), 0,
+                     st, g, tm, tn, per, f);
 }
-template <int MODE, class C>
+template <int MODE, class C, bool ACC32>
 void launch_fp4_multi(dim3 grid, hipStream_t st, const GemmFp4Batch& gb) {
-  hipLaunchKernelGGL((k_gemm_fp4_multi<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE>), grid, dim3(C::WM * C::WN * 64),
-                     0, st, gb);
+  hipLaunchKernelGGL((k_gemm_fp4_multi<MODE, C::WM, C::WN, C::TM, C::TN, C::WPE, ACC32>), grid,
+                     dim3(C::WM * C::WN * 64), 0, st, gb);
+}
+
+// The kernel of one launch: mode, tile form and accumulation.
+template <bool ACC32>
+void launch_fp4_kernel(GemmMode mode, bool wide, dim3 grid, hipStream_t st, const GemmFp4Batch& gb,
+                       const GemmFin& f) {
+  if (gb.count == 1) {
+    const GemmFp4Args& g = gb.p[0];
+    const int tm = gb.tiles_m[0], tn = gb.tiles_n[0];
+    const int64_t per = gb.tiles_per_mat[0];
+    switch (mode) {
+      case kModeGramA:
+        if (wide) launch_fp4_single<kModeGramA, Fp4Wide, ACC32>(grid, st, g, tm, tn, per, f);
+        else launch_fp4_single<kModeGramA, Fp4Narrow, ACC32>(grid, st, g, tm, tn, per, f);
+        break;
+      case kModeGramB: launch_fp4_single<kModeGramB, Fp4Narrow, ACC32>(grid, st, g, tm, tn, per, f); break;
+      default:
+        if (wide) launch_fp4_single<kModeUpdateX, Fp4Wide, ACC32>(grid, st, g, tm, tn, per, f);
+        else launch_fp4_single<kModeUpdateX, Fp4Narrow, ACC32>(grid, st, g, tm, tn, per, f);
+    }
+    return;
+  }
+  if (mode == kModeGramA) {
+    if (wide) launch_fp4_multi<kModeGramA, Fp4Wide, ACC32>(grid, st, gb);
+    else launch_fp4_multi<kModeGramA, Fp4Narrow, ACC32>(grid, st, gb);
+  } else {
+    launch_fp4_multi<kModeGramB, Fp4Narrow, ACC32>(grid, st, gb);
+  }
 }
 
 std::atomic<int> g_product_tiling{0};
@@ -695,6 +747,8 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
   if (count < 1 || count > kMaxGemmProblems) return hipErrorInvalidValue;
   if (fin && fin->count > 0 && (count != 1 || mode != kModeUpdateX || fin->count != list[0].batch))
     return hipErrorInvalidValue;
+  for (int i = 1; i < count; ++i)
+    if (list[i].acc32 != list[0].acc32) return hipErrorInvalidValue;   // one accumulation per launch
   // longest contraction first: its tiles take the longest, the short ones fill the tail
   int order[kMaxGemmProblems];
   for (int i = 0; i < count; ++i) order[i] = i;
@@ -721,32 +775,12 @@ hipError_t launch_gemm_fp4_batch(GemmMode mode, const GemmFp4Args* list, int cou
   const dim3 grid((uint32_t)total);
   const int forced = g_product_tiling.load(std::memory_order_relaxed);
   const bool wide = forced == 0 ? (total % kFp4Round == 0 || total >= kWideMinRounds * kFp4Round) : forced == 2;
-  if (gb.count == 1) {
-    GemmFin f;
-    if (fin) f = *fin;
-    const GemmFp4Args& g = gb.p[0];
-    const int tm = gb.tiles_m[0], tn = gb.tiles_n[0];
-    const int64_t per = gb.tiles_per_mat[0];
-    switch (mode) {
-      case kModeGramA:
-        if (wide) launch_fp4_single<kModeGramA, Fp4Wide>(grid, st, g, tm, tn, per, f);
-        else launch_fp4_single<kModeGramA, Fp4Narrow>(grid, st, g, tm, tn, per, f);
-        break;
-      case kModeGramB: launch_fp4_single<kModeGramB, Fp4Narrow>(grid, st, g, tm, tn, per, f); break;
-      default:
-        if (wide) launch_fp4_single<kModeUpdateX, Fp4Wide>(grid, st, g, tm, tn, per, f);
-        else launch_fp4_single<kModeUpdateX, Fp4Narrow>(grid, st, g, tm, tn, per, f);
-    }
-    return hipGetLastError();
-  }
   // several products per launch: the symmetric products only
-  if ((fin && fin->count > 0) || mode == kModeUpdateX) return hipErrorInvalidValue;
-  if (mode == kModeGramA) {
-    if (wide) launch_fp4_multi<kModeGramA, Fp4Wide>(grid, st, gb);
-    else launch_fp4_multi<kModeGramA, Fp4Narrow>(grid, st, gb);
-  } else {
-    launch_fp4_multi<kModeGramB, Fp4Narrow>(grid, st, gb);
-  }
+  if (gb.count > 1 && ((fin && fin->count > 0) || mode == kModeUpdateX)) return hipErrorInvalidValue;
+  GemmFin f;
+  if (fin) f = *fin;
+  if (gb.p[0].acc32) launch_fp4_kernel<true>(mode, wide, grid, st, gb, f);
+  else launch_fp4_kernel<false>(mode, wide, grid, st, gb, f);
   return hipGetLastError();
 }
 

@@ -237,6 +237,10 @@ struct GemmFp4Args {
   int64_t out_bstride;
   const float* aux;       // kModeGramB: A (may equal out); kModeUpdateX: X_k (may equal out)
   float ca, cb, cc;
+  // 0: exact products (binary32 rounding of the exact value, chained groups folded
+  // into binary64); 1: one binary32 MFMA accumulation over the whole contraction
+  // (every product of a launch takes the same value)
+  int acc32 = 0;
 };
 
 // kModeUpdateX, last step: when count > 0 the output goes to the callers' matrices

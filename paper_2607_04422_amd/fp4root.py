@@ -25,6 +25,7 @@ F_HADAMARD = 2
 F_ADAPTIVE46 = 4
 F_BF16_PATH = 8
 F_STOCHASTIC = 16
+F_FP32_ACCUM = 32   # products accumulate in binary32 (MFMA order) instead of exactly
 F_DEFAULT = 7
 
 
