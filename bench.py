@@ -313,6 +313,8 @@ def main():
     ap.add_argument("--no-bf16", action="store_true", help="skip the BF16 comparison path")
     ap.add_argument("--no-fp32-accum", action="store_true",
                     help="skip the NVFP4 path with binary32 product accumulation")
+    ap.add_argument("--probe-fp32-accum", action="store_true",
+                    help="with --probe: the calls use binary32 product accumulation (FP4ROOT_F_FP32_ACCUM)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the call")
@@ -347,7 +349,8 @@ def main():
     S = args.ns_steps
     flop = set_flop([(r, c) for (_, r, c) in shapes], S)
 
-    orth = F.Orthogonalizer(inputs, steps=S, flags=F.F_DEFAULT, clip_quantile=0.99, eps=1e-7, seed=0)
+    probe_flags = F.F_DEFAULT | (F.F_FP32_ACCUM if args.probe and args.probe_fp32_accum else 0)
+    orth = F.Orthogonalizer(inputs, steps=S, flags=probe_flags, clip_quantile=0.99, eps=1e-7, seed=0)
     orth()
     torch.cuda.synchronize()
     if orth.status() != 0:
