@@ -496,6 +496,42 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
       for (int j = 0; j < TN; ++j) p[i][j] = zero;
   }
 
+  // With binary32 accumulation the registers allow operand loads two stages ahead, in
+  // two register sets (even and odd stages).  The exact products load one stage ahead:
+  // their 32 x 64 form would spill, and their 64 x 64 form, which fits at 256 VGPRs,
+  // ran its update product 1-2 % slower that way.
+  constexpr bool kAhead2 = ACC32;
+  if constexpr (kAhead2) {
+    Fp4Stage<BM, NT> sa[2];
+    Fp4Stage<BN, NT> sb[2];
+    fp4_load<BM, NT>(src_a, nkb, 0, sa[0]);
+    fp4_load<BN, NT>(src_b, nkb, 0, sb[0]);
+    fp4_load<BM, NT>(src_a, nkb, 1, sa[1]);
+    fp4_load<BN, NT>(src_b, nkb, 1, sb[1]);
+    put(la0, lb0, sa[0], sb[0]);
+    fp4_load<BM, NT>(src_a, nkb, 2, sa[0]);
+    fp4_load<BN, NT>(src_b, nkb, 2, sb[0]);
+    if constexpr (!ACC32) fill_flags();
+    __syncthreads();
+    // pairs of stages, then an odd last stage after the loop (one exit, so the
+    // loop-carried chain registers keep their registers)
+    int s = 0;
+    for (; s + 1 < nstages; s += 2) {
+      run_single(stage_flags(s), la0, lb0);
+      put(la1, lb1, sa[1], sb[1]);
+      fp4_load<BM, NT>(src_a, nkb, s + 3, sa[1]);
+      fp4_load<BN, NT>(src_b, nkb, s + 3, sb[1]);
+      __syncthreads();
+      run_single(stage_flags(s + 1), la1, lb1);
+      if (s + 2 < nstages) {
+        put(la0, lb0, sa[0], sb[0]);
+        fp4_load<BM, NT>(src_a, nkb, s + 4, sa[0]);
+        fp4_load<BN, NT>(src_b, nkb, s + 4, sb[0]);
+      }
+      __syncthreads();
+    }
+    if (s < nstages) run_single(stage_flags(s), la0, lb0);
+  } else {
   Fp4Stage<BM, NT> sa;
   Fp4Stage<BN, NT> sb;
   fp4_load<BM, NT>(src_a, nkb, 0, sa);
@@ -528,6 +564,7 @@ FP4R_DEV void gemm_fp4_tile(const GemmFp4Args& g, int64_t wg, int tiles_m, int t
       fp4_load<BN, NT>(src_b, nkb, s + 3, sb);
     }
     __syncthreads();
+  }
   }
   if constexpr (ACC32) {
 #pragma unroll
