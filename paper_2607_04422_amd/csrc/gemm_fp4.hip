@@ -46,6 +46,13 @@
 // registers live beside the binary64 accumulators, which does not fit: every
 // arrangement tried spilled 36-200 binary32 registers per lane, at 32 x 64 per
 // wave (128 registers) and at 64 x 64 (256).
+//
+// Binary32 accumulation (GemmFp4Args::acc32, the library's FP4ROOT_F_FP32_ACCUM):
+// the same loop with one chain over the whole contraction (zeroed once, never
+// folded, no chain records), as tensor-core NVFP4 products accumulate in FP32.
+// Each product is then within the binary32 accumulation bound of its exact value
+// rather than equal to its rounding.  Its spare registers carry operand loads two
+// stages ahead.
 #include "device.h"
 #include "internal.h"
 
