@@ -53,6 +53,22 @@ def test_workspace_queries():
     assert lib.fp4root_orthogonalize_workspace(mats, 2, ctypes.byref(cfg)) > 0
     bad = F.NsConfig(5, None, 7 | 64, 0.99, 1e-7, 0)
     assert lib.fp4root_orthogonalize_workspace(mats, 2, ctypes.byref(bad)) == 0
+    # binary32 accumulation is an NVFP4-path option: accepted alone, rejected with the BF16 path
+    fp32 = F.NsConfig(5, None, 7 | F.F_FP32_ACCUM, 0.99, 1e-7, 0)
+    assert lib.fp4root_orthogonalize_workspace(mats, 2, ctypes.byref(fp32)) == \
+        lib.fp4root_orthogonalize_workspace(mats, 2, ctypes.byref(cfg))
+    both = F.NsConfig(5, None, F.F_CLIP | F.F_BF16_PATH | F.F_FP32_ACCUM, 0.99, 1e-7, 0)
+    assert lib.fp4root_orthogonalize_workspace(mats, 2, ctypes.byref(both)) == 0
+
+
+def test_product_tiling_switch():
+    """Host-side setting: returns the previous mode, rejects modes outside 0..2."""
+    lib = _lib()
+    assert lib.fp4root_set_product_tiling(1) == 0
+    assert lib.fp4root_set_product_tiling(2) == 1
+    assert lib.fp4root_set_product_tiling(3) == -1
+    assert lib.fp4root_set_product_tiling(-1) == -1
+    assert lib.fp4root_set_product_tiling(0) == 2
 
 
 def test_argument_errors_are_synchronous():
