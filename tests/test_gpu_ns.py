@@ -205,3 +205,64 @@ def test_graph_replay_equals_eager_call():
         assert orth.status() == 0
         other()                         # eager work between the replays
         torch.cuda.synchronize()
+
+
+def _degenerate_inputs():
+    """The method's degenerate inputs, each (name, matrix): zero, constant (rank 1, every
+    block tied), one non-zero entry (clipped away at p99), rank 1, zero rows and columns,
+    rows or columns spread over 2^+-40 (blocks far below the tensor maximum: E4M3 scales
+    that underflow or are subnormal), +-1 entries (ties of the 4/6 choice), the smallest
+    side (16, one block per row; tall), and inputs of extreme magnitude."""
+    rng = np.random.default_rng(2024)
+    cases = [("zero", np.zeros((64, 128), np.float32)),
+             ("constant", np.full((128, 256), 0.5, np.float32))]
+    m = np.zeros((64, 64), np.float32)
+    m[3, 17] = -2.5
+    cases.append(("single_entry", m))
+    u, v = rng.standard_normal(128), rng.standard_normal(384)
+    cases.append(("rank1", np.outer(u, v).astype(np.float32)))
+    m = rng.standard_normal((128, 256)).astype(np.float32)
+    m[::2] = 0.0
+    m[:, 64:80] = 0.0
+    cases.append(("zero_rows_cols", m))
+    cases.append(("range_rows", (rng.standard_normal((96, 192))
+                                 * np.exp2(rng.integers(-40, 41, size=(96, 1)))).astype(np.float32)))
+    cases.append(("range_cols", (rng.standard_normal((64, 256))
+                                 * np.exp2(rng.integers(-30, 31, size=(1, 256)))).astype(np.float32)))
+    cases.append(("signs", np.where(rng.random((112, 224)) < 0.5, -1.0, 1.0).astype(np.float32)))
+    cases.append(("side16", rng.standard_normal((16, 16)).astype(np.float32)))
+    cases.append(("tall_side16", rng.standard_normal((48, 16)).astype(np.float32)))
+    cases.append(("huge", (rng.standard_normal((64, 128)) * 1e30).astype(np.float32)))
+    cases.append(("tiny", (rng.standard_normal((80, 160)) * 1e-27).astype(np.float32)))
+    return cases
+
+
+@pytest.mark.parametrize("flags", ["default", "no_clip", "plain"])
+def test_orthogonalize_degenerate_inputs(flags):
+    # all in one call (eleven shape groups), the library's coefficients per shape; the
+    # products are exact, so every output equals the oracle's bit for bit
+    fl = {"default": F.F_DEFAULT, "no_clip": F.F_HADAMARD | F.F_ADAPTIVE46, "plain": 0}[flags]
+    cases = _degenerate_inputs()
+    ins = [torch.from_numpy(m).cuda() for _, m in cases]
+    orth = F.Orthogonalizer(ins, steps=5, flags=fl, seed=9)
+    outs = orth()
+    assert orth.status() == 0
+    for (name, m), o in zip(cases, outs):
+        co = F.fp4root_default_coeffs(m.shape[0], m.shape[1], 5)
+        ref = ns.orthogonalize(m, co, clip_on=bool(fl & F.F_CLIP), hadamard=bool(fl & F.F_HADAMARD),
+                               adaptive46=bool(fl & F.F_ADAPTIVE46), seed=9)
+        got = np_(o)
+        assert np.array_equal(got, ref), (name, int(np.count_nonzero(got != ref)))
+
+
+@pytest.mark.parametrize("scale", [1e-25, 1e-27, 1e-30])
+def test_ns_step_stages_extreme_scales(scale):
+    # normalised inputs of 1e-18 .. 1e-23 (the norm is far below eps): A and B hold
+    # binary32 subnormals, their tensor scales are subnormal (1e-27) or underflow to
+    # zero with a non-zero amax (1e-30); every stage still matches bit for bit
+    m = (np.random.default_rng(11).standard_normal((80, 160)) * scale).astype(np.float32)
+    x0, _, _ = ns.prepare(m)
+    a, b, c = F.fp4root_default_coeffs(80, 160, 5)[0]
+    x = torch.from_numpy(x0).cuda()
+    tr = F.fp4root_ns_step(x, a, b, c, flags=6, seed=31, step=0, trace=True)
+    _check_step(x0, a, b, c, 6, 31, 0, tr, np_(x))
