@@ -327,8 +327,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is a "
-                          "design note, not implemented", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "fp4root runs on one GPU only: sharding across GPUs is not "
+                          "implemented", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import numpy as np

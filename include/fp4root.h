@@ -60,7 +60,7 @@ enum {
   FP4ROOT_ERR_WORKSPACE = -3,   /* workspace null or smaller than the size query returned */
   FP4ROOT_ERR_NONFINITE = -4,   /* (device status) a NaN or Inf was met in an input */
   FP4ROOT_ERR_HIP = -5,         /* a HIP runtime call failed */
-  FP4ROOT_ERR_UNSUPPORTED = -6  /* a combination this build does not implement */
+  FP4ROOT_ERR_UNSUPPORTED = -6  /* a combination the library does not implement */
 };
 
 /* Flags. */
