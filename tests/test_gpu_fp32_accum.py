@@ -135,3 +135,27 @@ def test_fp32_accum_keeps_the_iterations_accuracy(which):
         assert torch.equal(b, c)                      # deterministic
         d = rel_fro(np_(b), np_(a))
         assert math.isfinite(d) and d <= 0.25, d      # same iteration, other rounding of the products
+
+
+def test_fp32_accum_grouped_call_equals_single_calls_and_replays():
+    """Each output is one binary32 chain in contraction order whatever the launch: a call over
+    six shape groups (grouped Gram launches, per-launch tile forms) gives every matrix the
+    bits of a call on that matrix alone, and a HIP-graph replay gives the eager call's bits."""
+    shapes = [(128, 256), (256, 128), (144, 144), (96, 400), (32, 1024), (272, 400), (128, 256)]
+    mats = [workloads.matrix(r, c, seed=70 + i, kind="normal_outliers") for i, (r, c) in enumerate(shapes)]
+    flags = F.F_DEFAULT | F.F_FP32_ACCUM
+    ins = [torch.from_numpy(m).cuda() for m in mats]
+    orth = F.Orthogonalizer(ins, steps=5, flags=flags, seed=4)
+    eager = [o.clone() for o in orth()]
+    assert orth.status() == 0
+    for i, m in enumerate(mats):
+        alone = F.fp4root_orthogonalize([torch.from_numpy(m).cuda()], steps=5, flags=flags, seed=4)[0]
+        assert torch.equal(alone, eager[i]), i
+    graph = orth.capture()
+    for r in range(3):
+        for o in orth.outputs:
+            o.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(eager, orth.outputs)):
+            assert torch.equal(a, b), (r, i)
